@@ -1,0 +1,348 @@
+"""Pins of the fp64 oracle to facts outside itself.
+
+Each ``pin_*`` function raises AssertionError when the oracle at ``lib`` is
+wrong.  They are collected by ``test_oracle_pins.py`` (the real oracle must
+pass all of them) and by ``test_oracle_mutations.py`` (every planted mistake
+must fail at least one).
+
+What pins what:
+
+* RoPE (rotate-half, theta_i = base^(-2i/D)):
+  - equals multiplication of the complex pairs (x_i + i*x_{i+D/2}) by
+    exp(i*p*theta_i) (numpy complex arithmetic);
+  - D=2: theta_0 = 1 for every base, so R(p) turns the plane by p radians;
+  - R(p) equals the matrix exponential of p times the rotation generator
+    (scipy.linalg.expm), the Lie-group definition of a rotation;
+  - R(-p) R(p) = I, and <R(p)q, R(p')k> = <q, R(p'-p)k>.
+* Projection: with RoPE off and identity alignment the operator reduces to a
+  textbook affine map, compared with numpy.matmul; it is linear in the KV
+  input (bias zero) for any configuration.
+* Alignment: equal-weight span pooling equals numpy's slice mean; a
+  per-channel constant input stays constant (partition of unity).
+* Identity translator (same shapes, same base, W = I, identity alignment)
+  returns its input exactly up to fp64 rounding.
+* Whole operator: on tiny shapes with spans, layer mixing, bias and RoPE on
+  both sides, the oracle equals a dense-matrix construction (expm rotations,
+  dense pooling matrix, numpy matmul) assembled independently here.
+* Input-feature order of a mixed target layer: W selecting feature
+  (j*Hs + h)*Ds + d returns source layer layer_map[l*mix+j], head h, dim d.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import scipy.linalg
+
+from oracle import oracle as O
+from paper_2608_30963_amd import synth as S
+
+TOL = 1e-11
+
+
+def _close(a, b, tol=TOL, what=""):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    assert a.shape == b.shape, (what, a.shape, b.shape)
+    # rows the operator leaves untouched are NaN on both sides
+    na, nb = np.isnan(a), np.isnan(b)
+    assert np.array_equal(na, nb), f"{what}: NaN pattern differs"
+    a, b = a[~na], b[~nb]
+    scale = max(1.0, float(np.abs(b).max()) if b.size else 1.0)
+    err = float(np.abs(a - b).max()) if a.size else 0.0
+    assert err <= tol * scale, f"{what}: max err {err:.3e} > {tol * scale:.3e}"
+
+
+def _theta(D, base):
+    return np.array([base ** (-2.0 * i / D) for i in range(D // 2)])
+
+
+def _generator(D, base):
+    """Skew-symmetric generator G with exp(pG) = rotate-half RoPE at p."""
+    h = D // 2
+    th = _theta(D, base)
+    G = np.zeros((D, D))
+    for i in range(h):
+        G[i + h, i] = th[i]
+        G[i, i + h] = -th[i]
+    return G
+
+
+def _rot_expm(D, base, p):
+    if base <= 0:
+        return np.eye(D)
+    return scipy.linalg.expm(p * _generator(D, base))
+
+
+# ---------------------------------------------------------------------------
+# RoPE
+# ---------------------------------------------------------------------------
+
+def pin_rope_complex(lib):
+    rng = np.random.default_rng(1)
+    for D, base in [(8, 1.0e4), (64, 1.0e4), (128, 1.0e6), (256, 1.0e4), (128, 5.0e5)]:
+        for p in [0.0, 1.0, 7.0, 4095.0, -123.0, 16383.0]:
+            x = rng.standard_normal(D)
+            h = D // 2
+            z = (x[:h] + 1j * x[h:]) * np.exp(1j * p * _theta(D, base))
+            want = np.concatenate([z.real, z.imag])
+            _close(O.rope(x, p, base, lib_path=lib), want, 1e-12, f"rope D={D} p={p}")
+
+
+def pin_rope_d2_closed_form(lib):
+    for base in [10.0, 1.0e4, 1.0e6]:
+        for p in [0.5, 1.0, 3.0, -2.0, 100.0]:
+            got = O.rope(np.array([1.0, 0.0]), p, base, lib_path=lib)
+            _close(got, [math.cos(p), math.sin(p)], 1e-14, "D=2 e0")
+            got = O.rope(np.array([0.0, 1.0]), p, base, lib_path=lib)
+            _close(got, [-math.sin(p), math.cos(p)], 1e-14, "D=2 e1")
+
+
+def pin_rope_expm(lib):
+    rng = np.random.default_rng(2)
+    for D, base in [(4, 100.0), (8, 1.0e4), (16, 5.0e5)]:
+        for p in [1.0, 5.0, 37.0, -9.0]:
+            x = rng.standard_normal(D)
+            _close(O.rope(x, p, base, lib_path=lib), _rot_expm(D, base, p) @ x, 1e-9,
+                   f"expm D={D}")
+
+
+def pin_rope_group(lib):
+    rng = np.random.default_rng(3)
+    D, base = 128, 1.0e6
+    q = rng.standard_normal(D)
+    k = rng.standard_normal(D)
+    for p, pp in [(5.0, 17.0), (1000.0, 3.0), (4000.0, 4095.0)]:
+        back = O.rope(O.rope(q, p, base, lib_path=lib), -p, base, lib_path=lib)
+        _close(back, q, 1e-12, "R(-p)R(p)")
+        lhs = O.rope(q, p, base, lib_path=lib) @ O.rope(k, pp, base, lib_path=lib)
+        rhs = q @ O.rope(k, pp - p, base, lib_path=lib)
+        assert abs(lhs - rhs) <= 1e-10 * max(1.0, abs(rhs)), (lhs, rhs)
+
+
+# ---------------------------------------------------------------------------
+# Whole operator
+# ---------------------------------------------------------------------------
+
+def _f64(x, dtype):
+    return S.storage_to_f32(x, dtype).astype(np.float64)
+
+
+def pin_identity_translator(lib):
+    for dtype in (S.F32, S.BF16):
+        m = S.ModelShape(3, 2, 16, 1.0e4)
+        spec = S.tiny_spec(src=m, tgt=m, layer_map=(0, 1, 2), dtype=dtype, src_tokens=21,
+                           batch=2)
+        p = S.make_problem(spec)
+        eye = np.broadcast_to(np.eye(32, dtype=np.float32), (3, 32, 32))
+        p.w_k = S.to_storage(eye, dtype)
+        p.w_v = p.w_k.copy()
+        tk, tv = O.translate(p, lib_path=lib)
+        _close(tk, _f64(p.src_k, dtype), 1e-12, "identity K")
+        _close(tv, _f64(p.src_v, dtype), 0.0, "identity V")
+
+
+def _no_rope_matmul_expect(p):
+    """Per target layer: concat mixed source layers/heads, matmul with W^T, + b."""
+    spec = p.spec
+    Ls, Hs, Ds = spec.src.n_layers, spec.src.n_kv_heads, spec.src.head_dim
+    Lt, Ht, Dt = spec.tgt.n_layers, spec.tgt.n_kv_heads, spec.tgt.head_dim
+    B, T = spec.batch, spec.src_tokens
+    outs = []
+    for src, w, bias in ((p.src_k, p.w_k, p.b_k), (p.src_v, p.w_v, p.b_v)):
+        x = _f64(src, spec.dtype)                       # [Ls, B, Hs, T, Ds]
+        W = _f64(w, spec.dtype)                         # [Lt, out, in]
+        res = np.empty((Lt, B, Ht, T, Dt))
+        for l in range(Lt):
+            layers = [spec.layer_map[l * spec.mix + j] for j in range(spec.mix)]
+            # [B, T, mix, Hs, Ds] -> [B, T, in]
+            z = np.stack([x[ls] for ls in layers], axis=0).transpose(1, 3, 0, 2, 4)
+            z = z.reshape(B, T, spec.d_in)
+            u = np.matmul(z, W[l].T)
+            if bias is not None:
+                u = u + bias[l].astype(np.float64)
+            res[l] = u.reshape(B, T, Ht, Dt).transpose(0, 2, 1, 3)
+        outs.append(res)
+    return outs
+
+
+def pin_no_rope_is_matmul(lib):
+    for mix, lmap in [(1, (2, 0)), (2, (1, 2, 0, 0))]:
+        src = S.ModelShape(3, 2, 8, 0.0)
+        tgt = S.ModelShape(2, 3, 4, 0.0)
+        spec = S.tiny_spec(src=src, tgt=tgt, mix=mix, layer_map=lmap, bias_std=0.5,
+                           dtype=S.BF16)
+        p = S.make_problem(spec)
+        tk, tv = O.translate(p, lib_path=lib)
+        ek, ev = _no_rope_matmul_expect(p)
+        _close(tk, ek, 1e-12, f"matmul K mix={mix}")
+        _close(tv, ev, 1e-12, f"matmul V mix={mix}")
+
+
+def pin_linearity(lib):
+    # integer-valued inputs and coefficients keep a*X + b*Y exact in float32
+    spec = S.tiny_spec(span_lo=1, span_hi=3, src_tokens=13, mix=2, layer_map=(0, 1, 2, 2))
+    p1 = S.make_problem(spec)
+    p2 = S.make_problem(spec)       # same translator and alignment, other KV
+    other = S.make_problem(spec.replace(seed=7))
+    p2.src_k, p2.src_v = other.src_k, other.src_v
+    for q in (p1, p2):
+        q.src_k = np.round(q.src_k * 8).astype(np.float32)
+        q.src_v = np.round(q.src_v * 8).astype(np.float32)
+    a, b = 3.0, -2.0
+    p3 = S.make_problem(spec)
+    p3.src_k = (a * p1.src_k + b * p2.src_k).astype(np.float32)
+    p3.src_v = (a * p1.src_v + b * p2.src_v).astype(np.float32)
+    k1, v1 = O.translate(p1, lib_path=lib)
+    k2, v2 = O.translate(p2, lib_path=lib)
+    k3, v3 = O.translate(p3, lib_path=lib)
+    _close(k3, a * k1 + b * k2, 1e-10, "linear K")
+    _close(v3, a * v1 + b * v2, 1e-10, "linear V")
+
+
+def pin_span_mean(lib):
+    src = S.ModelShape(2, 2, 4, 0.0)
+    spec = S.tiny_spec(src=src, tgt=S.ModelShape(2, 2, 4, 0.0), layer_map=(1, 0),
+                       span_lo=1, span_hi=3, src_tokens=17, batch=3)
+    p = S.make_problem(spec)
+    eye = np.broadcast_to(np.eye(8, dtype=np.float32), (2, 8, 8)).copy()
+    p.w_k = eye
+    p.w_v = eye
+    tk, tv = O.translate(p, lib_path=lib)
+    for b in range(spec.batch):
+        lens = S.draw_spans(spec, b)
+        starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+        for l in range(2):
+            ls = spec.layer_map[l]
+            for t, (s0, n) in enumerate(zip(starts, lens)):
+                for src, got in ((p.src_k, tk), (p.src_v, tv)):
+                    want = src[ls, b, :, s0:s0 + n, :].astype(np.float64).mean(axis=1)
+                    # the stored weights are float32(1/n), not exactly 1/n
+                    _close(got[l, b, :, t, :], want, 1e-7, "span mean")
+
+
+def pin_partition_of_unity(lib):
+    spec = S.tiny_spec(src=S.ModelShape(1, 1, 6, 0.0), tgt=S.ModelShape(1, 1, 6, 0.0),
+                       layer_map=(0,), span_lo=1, span_hi=3, src_tokens=40, batch=2)
+    p = S.make_problem(spec)
+    c = np.arange(1, 7, dtype=np.float32)
+    p.src_k = np.broadcast_to(c, p.src_k.shape).copy()
+    p.src_v = np.broadcast_to(-c, p.src_v.shape).copy()
+    p.w_k = np.eye(6, dtype=np.float32)[None].copy()
+    p.w_v = p.w_k.copy()
+    tk, tv = O.translate(p, lib_path=lib)
+    for b in range(spec.batch):
+        T = int(p.tgt_tokens[b])
+        _close(tk[0, b, 0, :T], np.broadcast_to(c, (T, 6)), 1e-7, "const K")
+        _close(tv[0, b, 0, :T], np.broadcast_to(-c, (T, 6)), 1e-7, "const V")
+
+
+def _dense_expect(p):
+    """Independent construction: expm rotations, dense pooling matrix,
+    matmul projection, expm target rotation."""
+    spec = p.spec
+    Hs, Ds = spec.src.n_kv_heads, spec.src.head_dim
+    Lt, Ht, Dt = spec.tgt.n_layers, spec.tgt.n_kv_heads, spec.tgt.head_dim
+    B, T = spec.batch, spec.src_tokens
+    cap = int(p.tgt_tokens.max())
+    ek = np.full((Lt, B, Ht, cap, Dt), np.nan)
+    ev = np.full((Lt, B, Ht, cap, Dt), np.nan)
+    xk = _f64(p.src_k, spec.dtype)
+    xv = _f64(p.src_v, spec.dtype)
+    Wk = _f64(p.w_k, spec.dtype)
+    Wv = _f64(p.w_v, spec.dtype)
+    Rs = [_rot_expm(Ds, spec.src.rope_base, -k) for k in range(T)]
+    Rt = [_rot_expm(Dt, spec.tgt.rope_base, t) for t in range(cap)]
+    row0 = 0
+    for b in range(B):
+        Tt = int(p.tgt_tokens[b])
+        P = np.zeros((Tt, T))
+        if p.row_ptr is None:
+            P = np.eye(T)
+        else:
+            for t in range(Tt):
+                for e in range(p.row_ptr[row0 + t], p.row_ptr[row0 + t + 1]):
+                    P[t, p.col_idx[e]] += float(p.weight[e])
+        for l in range(Lt):
+            zk = np.zeros((T, spec.d_in))
+            zv = np.zeros((T, spec.d_in))
+            for j in range(spec.mix):
+                ls = spec.layer_map[l * spec.mix + j]
+                for h in range(Hs):
+                    c0 = (j * Hs + h) * Ds
+                    for k in range(T):
+                        zk[k, c0:c0 + Ds] = Rs[k] @ xk[ls, b, h, k]
+                    zv[:, c0:c0 + Ds] = xv[ls, b, h]
+            uk = P @ zk @ Wk[l].T
+            uv = P @ zv @ Wv[l].T
+            if p.b_k is not None:
+                uk += p.b_k[l]
+                uv += p.b_v[l]
+            for h in range(Ht):
+                for t in range(Tt):
+                    ek[l, b, h, t] = Rt[t] @ uk[t, h * Dt:(h + 1) * Dt]
+                ev[l, b, h, :Tt] = uv[:, h * Dt:(h + 1) * Dt]
+        row0 += Tt
+    return ek, ev
+
+
+def pin_dense_bruteforce(lib):
+    cases = [
+        dict(src=S.ModelShape(3, 1, 4, 100.0), tgt=S.ModelShape(2, 2, 2, 10.0), mix=2,
+             layer_map=(0, 2, 1, 1), span_lo=1, span_hi=3, src_tokens=5, batch=2,
+             bias_std=0.3),
+        dict(src=S.ModelShape(2, 2, 6, 1.0e4), tgt=S.ModelShape(3, 1, 8, 500.0), mix=1,
+             layer_map=(1, 0, 1), src_tokens=7, batch=1, bias_std=0.0, dtype=S.BF16),
+        dict(src=S.ModelShape(4, 2, 4, 50.0), tgt=S.ModelShape(2, 2, 4, 0.0), mix=3,
+             layer_map=(0, 1, 2, 1, 2, 3), span_lo=1, span_hi=2, src_tokens=6, batch=2),
+    ]
+    for kw in cases:
+        spec = S.tiny_spec(**kw)
+        p = S.make_problem(spec)
+        tk, tv = O.translate(p, lib_path=lib)
+        ek, ev = _dense_expect(p)
+        _close(tk, ek, 1e-9, f"dense K {kw}")
+        _close(tv, ev, 1e-9, f"dense V {kw}")
+
+
+def pin_mixed_feature_order(lib):
+    src = S.ModelShape(4, 3, 4, 0.0)
+    tgt = S.ModelShape(1, 1, 4, 0.0)
+    lmap = (3, 0, 2)
+    spec = S.tiny_spec(src=src, tgt=tgt, mix=3, layer_map=lmap, src_tokens=5, batch=2)
+    p = S.make_problem(spec)
+    for j in range(3):
+        for h in range(3):
+            W = np.zeros((1, 4, spec.d_in), dtype=np.float32)
+            for d in range(4):
+                W[0, d, (j * 3 + h) * 4 + d] = 1.0
+            p.w_k = W
+            p.w_v = W
+            tk, tv = O.translate(p, lib_path=lib)
+            _close(tk[0, :, 0], p.src_k[lmap[j], :, h].astype(np.float64), 0.0, "sel K")
+            _close(tv[0, :, 0], p.src_v[lmap[j], :, h].astype(np.float64), 0.0, "sel V")
+
+
+def pin_rows_match_translate(lib):
+    spec = S.tiny_spec(span_lo=1, span_hi=3, src_tokens=11, batch=3, bias_std=0.2)
+    p = S.make_problem(spec)
+    tk, tv = O.translate(p, lib_path=lib)
+    rng = np.random.default_rng(5)
+    L, Bs, Ts = [], [], []
+    for _ in range(20):
+        b = int(rng.integers(spec.batch))
+        L.append(int(rng.integers(spec.tgt.n_layers)))
+        Bs.append(b)
+        Ts.append(int(rng.integers(p.tgt_tokens[b])))
+    rk, rv = O.rows(p, L, Bs, Ts, lib_path=lib)
+    for i, (l, b, t) in enumerate(zip(L, Bs, Ts)):
+        _close(rk[i], tk[l, b, :, t, :].reshape(-1), 0.0, "rows K")
+        _close(rv[i], tv[l, b, :, t, :].reshape(-1), 0.0, "rows V")
+
+
+ALL_PINS = [
+    pin_rope_complex, pin_rope_d2_closed_form, pin_rope_expm, pin_rope_group,
+    pin_identity_translator, pin_no_rope_is_matmul, pin_linearity, pin_span_mean,
+    pin_partition_of_unity, pin_dense_bruteforce, pin_mixed_feature_order,
+    pin_rows_match_translate,
+]
