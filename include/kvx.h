@@ -1,0 +1,151 @@
+/*
+ * kvx.h -- C-ABI of the cross-model KV-translation library (gfx950 / MI355X).
+ *
+ * The operator turns a source model's per-layer KV cache for a context into
+ * the KV cache of a different target model, so the target can decode without
+ * its own prefill:  KV^_B(C) = T_{A->B}(KV_A(C))  (paper Section 4, the
+ * translation operator), with T = T_theta a parameterised translator
+ * (Section 5).  Translation may work per layer or on groups of layers and per
+ * KV head (Section 5, granularity), and source and target may differ in
+ * layers, heads, hidden size and tokenizer (Section 4).  Concretely, for target
+ * layer l, context b, target token t:
+ *
+ *   x_k  = concat_{j<mix, h<Hs} R_src(-k) K_src[layer_map[l*mix+j]][b][h][k]
+ *          (V: the same concatenation without the rotation)
+ *   z_t  = sum_{e in row t} weight[e] * x_{col_idx[e]}     (identity: z_t = x_t)
+ *   u    = W[l] z_t + bias[l]
+ *   K_tgt[l][b][h][t] = R_tgt(+t) u[h*Dt : (h+1)*Dt],   V_tgt: u[h*Dt : (h+1)*Dt]
+ *
+ * R(p) is rotate-half RoPE: the pair (i, i + D/2) of a head vector turns by
+ * p * theta_i, theta_i = base^(-2i/D).  Positions are 0-based within each
+ * context.  The translator's learned parameters theta of Section 5 are W and
+ * bias, one pair per target layer and per K/V.
+ *
+ * Everything of the translation runs in HIP kernels on the caller's stream;
+ * the host side validates, sizes the launch and enqueues.
+ */
+#ifndef KVX_H
+#define KVX_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes.  No function throws across the ABI. */
+typedef enum {
+  KVX_OK = 0,
+  KVX_EINVAL = 1,       /* NULL or out-of-range argument */
+  KVX_ESHAPE = 2,       /* inconsistent dimensions, strides or capacity */
+  KVX_EUNSUPPORTED = 3, /* valid but not supported by this build (e.g. odd head_dim) */
+  KVX_ENOMEM = 4,       /* device allocation failed */
+  KVX_EHIP = 5,         /* a HIP runtime call failed; see kvx_last_hip_error() */
+  KVX_EDATA = 6         /* device CSR contents invalid (validation mode only) */
+} kvx_status;
+
+/* Storage dtype of KV tensors and translator weights. */
+typedef enum { KVX_F32 = 0, KVX_BF16 = 1 } kvx_dtype;
+
+/* Precision of the matrix-core operands (bf16 plans only; ignored for f32).
+ *  KVX_PREC_BF16X2: a computed operand (RoPE-de-rotated K, pooled rows with
+ *                   non-unit weights) is split a = hi + lo into two bf16
+ *                   values and contracted twice against the same bf16 W;
+ *                   operands that are already bf16 go through once.  Default.
+ *  KVX_PREC_BF16:   every operand rounded once to bf16.
+ * Accumulation is fp32 in every mode. */
+typedef enum { KVX_PREC_BF16X2 = 0, KVX_PREC_BF16 = 1 } kvx_precision;
+
+/* One side of the translation (a model's KV-cache geometry). */
+typedef struct {
+  int32_t n_layers;        /* transformer layers */
+  int32_t n_kv_heads;      /* KV heads per layer */
+  int32_t head_dim;        /* even */
+  double rope_base;        /* RoPE base; <= 0 disables RoPE on this side */
+  const double* inv_freq;  /* optional host [head_dim/2], overrides base^(-2i/D);
+                              copied by kvx_plan_create */
+} kvx_model;
+
+/* Translator and geometry; consumed once by kvx_plan_create. */
+typedef struct {
+  kvx_model src;
+  kvx_model tgt;
+  int32_t mix;               /* source layers concatenated per target layer, >= 1 */
+  const int32_t* layer_map;  /* host [tgt.n_layers * mix], source layer ids;
+                                input feature (j*Hs + h)*Ds + d of target layer l
+                                is source layer layer_map[l*mix+j], head h, dim d */
+  int32_t dtype;             /* kvx_dtype of KV tensors and weights */
+  const void* w_k;           /* device [Lt][Ht*Dt][mix*Hs*Ds], nn.Linear [out][in] order */
+  const void* w_v;
+  const float* b_k;          /* device fp32 [Lt][Ht*Dt], or NULL for zero bias */
+  const float* b_v;
+  int32_t precision;         /* kvx_precision */
+} kvx_plan_desc;
+
+/* One translation call.  Strides are in elements, for (layer, batch, head,
+ * token); head_dim is unit-stride.  All-zero strides mean the contiguous
+ * layout [L][B][H][T][D] (src: T = src_tokens; tgt: T = tgt_capacity). */
+typedef struct {
+  int32_t batch;             /* B independent contexts */
+  int32_t src_tokens;        /* T_s, the same for all contexts */
+  const void* src_k;         /* device, [Ls][B][Hs][T_s][Ds] */
+  const void* src_v;
+  int64_t src_stride[4];
+  /* Token alignment (tokenizers differ).  tgt_tokens == NULL means identity
+   * alignment: T_t = T_s and the CSR pointers are ignored. */
+  const int32_t* tgt_tokens; /* host [B], T_t of each context */
+  const int32_t* row_ptr;    /* device [R+1], R = sum T_t; rows concatenated per
+                                context, row_ptr[0] = 0 */
+  const int32_t* col_idx;    /* device [nnz], source token index within the context */
+  const float* weight;       /* device [nnz], pooling weights */
+  void* tgt_k;               /* device, [Lt][B][Ht][tgt_capacity][Dt] */
+  void* tgt_v;
+  int64_t tgt_stride[4];
+  int32_t tgt_capacity;      /* >= max_b T_t[b]; rows t >= T_t[b] are left untouched */
+} kvx_io;
+
+typedef struct kvx_plan kvx_plan;
+
+/* Validate the descriptor, copy the layer map and RoPE tables, and repack the
+ * weights into plan-owned device memory (synchronous; uses the current HIP
+ * device).  The caller's weight and bias buffers may be freed on return.
+ * Errors: KVX_EINVAL (NULL/out of range), KVX_ESHAPE, KVX_EUNSUPPORTED
+ * (head_dim odd), KVX_ENOMEM, KVX_EHIP.  On error *out is set to NULL. */
+kvx_status kvx_plan_create(const kvx_plan_desc* desc, kvx_plan** out);
+
+/* Enqueue the translation on `stream` (a hipStream_t; NULL = default stream).
+ * Asynchronous: KV and alignment buffers are borrowed and must stay valid
+ * until the stream work completes.  Every host-visible argument is validated
+ * before anything is enqueued; device-resident CSR contents are trusted unless
+ * the environment sets KVX_VALIDATE=1 (then they are copied back and checked:
+ * monotone row_ptr, col_idx in range; KVX_EDATA otherwise).  batch == 0 or an
+ * empty output is a no-op returning KVX_OK.  The plan is immutable and holds no
+ * per-call scratch, so concurrent calls on different streams are safe. */
+kvx_status kvx_translate(const kvx_plan* plan, const kvx_io* io, void* stream);
+
+/* Release a plan (NULL-safe).  The caller must ensure no translation that uses
+ * it is still running. */
+void kvx_plan_destroy(kvx_plan* plan);
+
+/* Static description of a status code. */
+const char* kvx_status_string(kvx_status s);
+
+/* Last HIP error code seen by this thread (0 if none). */
+int32_t kvx_last_hip_error(void);
+
+/* Which kernel a plan dispatches to and its launch shape (diagnostics). */
+typedef struct {
+  int32_t kernel;        /* 0 = fp32 tiled kernel, 1 = bf16 MFMA fused kernel */
+  int32_t tile_rows;     /* target rows per workgroup */
+  int32_t tile_cols;     /* output features per workgroup */
+  int32_t threads;       /* threads per workgroup */
+  int32_t split_k;       /* 1 when K operands are split hi/lo (BF16X2) */
+  int64_t weight_bytes;  /* device bytes held by the plan */
+} kvx_plan_info;
+
+kvx_status kvx_plan_query(const kvx_plan* plan, kvx_plan_info* info);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KVX_H */

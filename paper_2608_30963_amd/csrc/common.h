@@ -1,0 +1,74 @@
+// common.h -- device helpers shared by the kvx kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvx {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef uint16_t bf16_t;  // storage: bfloat16 bit pattern
+
+// Contexts handled by one launch; larger batches are split by the host.
+constexpr int kMaxBatch = 64;
+
+// Per-launch description of the contexts (passed by value as a kernel argument).
+struct BatchArgs {
+  int32_t n;                       // contexts in this launch
+  int32_t tile_start[kMaxBatch + 1];  // prefix sum of row tiles per context
+  int32_t t_tgt[kMaxBatch];        // T_t of each context
+  int32_t row_base[kMaxBatch];     // first CSR row of each context
+};
+
+struct Strides {
+  int64_t l, b, h, t;  // elements; head_dim is unit-stride
+};
+
+// Exact widening of a bfloat16 bit pattern.
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// float -> bfloat16, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float load_f32(const T* p);
+template <> __device__ __forceinline__ float load_f32<float>(const float* p) { return *p; }
+template <> __device__ __forceinline__ float load_f32<bf16_t>(const bf16_t* p) {
+  return bf16_to_f32(*p);
+}
+
+template <typename T> __device__ __forceinline__ T store_cvt(float f);
+template <> __device__ __forceinline__ float store_cvt<float>(float f) { return f; }
+template <> __device__ __forceinline__ bf16_t store_cvt<bf16_t>(float f) {
+  return f32_to_bf16(f);
+}
+
+// cos and sin of the RoPE angle pos * theta, given f = theta / (2*pi) in fp64.
+// The angle is formed and reduced to [-1/2, 1/2] revolutions in fp64, so its
+// error does not grow with the position; the hardware sine/cosine (argument
+// in revolutions) then evaluates the reduced angle (measured on gfx950 over
+// [-1/2, 1/2]: max abs error 1.2e-7 against fp64).
+__device__ __forceinline__ void rope_cs(double f, int32_t pos, float& c, float& s) {
+  double r = static_cast<double>(pos) * f;
+  r -= rint(r);
+  float x = static_cast<float>(r);
+  s = __builtin_amdgcn_sinf(x);
+  c = __builtin_amdgcn_cosf(x);
+}
+
+// Which context a linear row-tile index belongs to (batch is small).
+__device__ __forceinline__ int find_context(const BatchArgs& ba, int tile) {
+  int b = 0;
+  while (b + 1 < ba.n && ba.tile_start[b + 1] <= tile) ++b;
+  return b;
+}
+
+}  // namespace kvx

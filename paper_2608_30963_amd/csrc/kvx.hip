@@ -1,0 +1,430 @@
+// kvx.hip -- C-ABI of the KV-translation library: plan creation (validation,
+// weight packing, RoPE tables), translation (validation, launch), teardown.
+// The declarations and their contracts are in include/kvx.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "kvx.h"
+#include "common.h"
+#include "kernel_mfma.h"
+#include "kernel_tiled.h"
+
+using namespace kvx;
+
+namespace {
+
+thread_local int32_t g_last_hip = 0;
+
+kvx_status hip_fail(hipError_t e) {
+  g_last_hip = static_cast<int32_t>(e);
+  return e == hipErrorOutOfMemory ? KVX_ENOMEM : KVX_EHIP;
+}
+
+#define KVX_HIP(x)                          \
+  do {                                      \
+    hipError_t e_ = (x);                    \
+    if (e_ != hipSuccess) return hip_fail(e_); \
+  } while (0)
+
+enum Kernel { kTiled = 0, kFused = 1 };
+
+}  // namespace
+
+struct kvx_plan {
+  int device = 0;
+  kvx_model src{}, tgt{};
+  int32_t mix = 1;
+  int32_t dtype = KVX_BF16;
+  int32_t precision = KVX_PREC_BF16X2;
+  int32_t din = 0, dout = 0;
+  int kernel = kTiled;
+  int64_t bytes = 0;
+  // device memory owned by the plan
+  int32_t* layer_map = nullptr;  // [Lt*mix]
+  double* fs = nullptr;          // [Ds/2] theta_i / 2pi (zeros when RoPE is off)
+  double* ft = nullptr;          // [Dt/2]
+  void* w[2] = {nullptr, nullptr};  // tiled: [Lt][dout][din]; fused: packed fragments
+  float* bias[2] = {nullptr, nullptr};
+  void* block = nullptr;         // single allocation backing all of the above
+};
+
+namespace {
+
+bool valid_model(const kvx_model& m) {
+  return m.n_layers > 0 && m.n_kv_heads > 0 && m.head_dim > 0 && std::isfinite(m.rope_base);
+}
+
+// theta_i / (2 pi) for i < D/2 in fp64; all zero when the side has no RoPE.
+std::vector<double> rope_table(const kvx_model& m) {
+  std::vector<double> f(m.head_dim / 2, 0.0);
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int i = 0; i < m.head_dim / 2; ++i) {
+    double th = 0.0;
+    if (m.inv_freq)
+      th = m.inv_freq[i];
+    else if (m.rope_base > 0.0)
+      th = std::pow(m.rope_base, -2.0 * i / m.head_dim);
+    f[i] = th / two_pi;
+  }
+  return f;
+}
+
+bool fused_supported(const kvx_plan& p) {
+  const int ds = p.src.head_dim;
+  return p.dtype == KVX_BF16 && (ds == 64 || ds == 128 || ds == 256) &&
+         p.tgt.head_dim % 64 == 0 && p.dout % 64 == 0 && p.din % 16 == 0;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+}  // namespace
+
+extern "C" {
+
+const char* kvx_status_string(kvx_status s) {
+  switch (s) {
+    case KVX_OK: return "ok";
+    case KVX_EINVAL: return "invalid argument";
+    case KVX_ESHAPE: return "inconsistent shape, stride or capacity";
+    case KVX_EUNSUPPORTED: return "unsupported configuration";
+    case KVX_ENOMEM: return "out of device memory";
+    case KVX_EHIP: return "HIP runtime error";
+    case KVX_EDATA: return "invalid alignment data";
+  }
+  return "unknown status";
+}
+
+int32_t kvx_last_hip_error(void) { return g_last_hip; }
+
+kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
+  if (out) *out = nullptr;
+  if (!d || !out || !d->layer_map || !d->w_k || !d->w_v) return KVX_EINVAL;
+  if (!valid_model(d->src) || !valid_model(d->tgt) || d->mix < 1) return KVX_EINVAL;
+  if (d->dtype != KVX_F32 && d->dtype != KVX_BF16) return KVX_EINVAL;
+  if (d->precision != KVX_PREC_BF16X2 && d->precision != KVX_PREC_BF16) return KVX_EINVAL;
+  if (d->src.head_dim % 2 || d->tgt.head_dim % 2) return KVX_EUNSUPPORTED;
+  const int64_t lt = d->tgt.n_layers;
+  for (int64_t i = 0; i < lt * d->mix; ++i)
+    if (d->layer_map[i] < 0 || d->layer_map[i] >= d->src.n_layers) return KVX_EINVAL;
+  const int64_t din64 = int64_t(d->mix) * d->src.n_kv_heads * d->src.head_dim;
+  const int64_t dout64 = int64_t(d->tgt.n_kv_heads) * d->tgt.head_dim;
+  if (din64 > (1 << 20) || dout64 > (1 << 20)) return KVX_ESHAPE;
+  if (d->src.inv_freq)
+    for (int i = 0; i < d->src.head_dim / 2; ++i)
+      if (!std::isfinite(d->src.inv_freq[i])) return KVX_EINVAL;
+  if (d->tgt.inv_freq)
+    for (int i = 0; i < d->tgt.head_dim / 2; ++i)
+      if (!std::isfinite(d->tgt.inv_freq[i])) return KVX_EINVAL;
+
+  kvx_plan* p = new (std::nothrow) kvx_plan();
+  if (!p) return KVX_ENOMEM;
+  p->src = d->src;
+  p->tgt = d->tgt;
+  p->src.inv_freq = p->tgt.inv_freq = nullptr;  // tables live on the device
+  p->mix = d->mix;
+  p->dtype = d->dtype;
+  p->precision = d->precision;
+  p->din = static_cast<int32_t>(din64);
+  p->dout = static_cast<int32_t>(dout64);
+  p->kernel = fused_supported(*p) ? kFused : kTiled;
+
+  auto fail = [&](kvx_status s) {
+    kvx_plan_destroy(p);
+    return s;
+  };
+
+  hipError_t e = hipGetDevice(&p->device);
+  if (e != hipSuccess) return fail(hip_fail(e));
+
+  const size_t esz = d->dtype == KVX_F32 ? 4 : 2;
+  const size_t wbytes = size_t(lt) * dout64 * din64 * esz;
+  const size_t bbytes = size_t(lt) * dout64 * sizeof(float);
+  const size_t mbytes = size_t(lt) * d->mix * sizeof(int32_t);
+  const size_t fsb = d->src.head_dim / 2 * sizeof(double);
+  const size_t ftb = d->tgt.head_dim / 2 * sizeof(double);
+  size_t off_w0 = 0, off_w1 = align256(wbytes), off_b0 = off_w1 + align256(wbytes);
+  size_t off_b1 = off_b0 + align256(bbytes), off_m = off_b1 + align256(bbytes);
+  size_t off_fs = off_m + align256(mbytes), off_ft = off_fs + align256(fsb);
+  size_t total = off_ft + align256(ftb);
+  e = hipMalloc(&p->block, total);
+  if (e != hipSuccess) return fail(hip_fail(e));
+  p->bytes = static_cast<int64_t>(total);
+  char* base = static_cast<char*>(p->block);
+  p->w[0] = base + off_w0;
+  p->w[1] = base + off_w1;
+  p->bias[0] = reinterpret_cast<float*>(base + off_b0);
+  p->bias[1] = reinterpret_cast<float*>(base + off_b1);
+  p->layer_map = reinterpret_cast<int32_t*>(base + off_m);
+  p->fs = reinterpret_cast<double*>(base + off_fs);
+  p->ft = reinterpret_cast<double*>(base + off_ft);
+
+  // Weights: copy to the host, repack, upload.  Plan creation is once per
+  // translator, so clarity wins over speed here.
+  std::vector<char> host(wbytes), packed;
+  const void* wsrc[2] = {d->w_k, d->w_v};
+  for (int kv = 0; kv < 2; ++kv) {
+    e = hipMemcpy(host.data(), wsrc[kv], wbytes, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail(hip_fail(e));
+    const void* up = host.data();
+    if (p->kernel == kFused) {
+      // B fragment (n-block nb, k-step ks) of v_mfma_f32_32x32x16_bf16: lane
+      // holds W[nb*32 + lane%32][ks*16 + 8*(lane/32) + j], j < 8.
+      packed.resize(wbytes);
+      const uint16_t* wsrc16 = reinterpret_cast<const uint16_t*>(host.data());
+      uint16_t* dst = reinterpret_cast<uint16_t*>(packed.data());
+      const int64_t nb_n = dout64 / 32, ks_n = din64 / 16;
+      for (int64_t l = 0; l < lt; ++l)
+        for (int64_t nb = 0; nb < nb_n; ++nb)
+          for (int64_t ks = 0; ks < ks_n; ++ks)
+            for (int lanei = 0; lanei < 64; ++lanei)
+              for (int jj = 0; jj < 8; ++jj) {
+                const int64_t o = nb * 32 + lanei % 32;
+                const int64_t i = ks * 16 + 8 * (lanei / 32) + jj;
+                dst[((((l * nb_n + nb) * ks_n + ks) * 64 + lanei) * 8) + jj] =
+                    wsrc16[(l * dout64 + o) * din64 + i];
+              }
+      up = packed.data();
+    }
+    e = hipMemcpy(p->w[kv], up, wbytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(hip_fail(e));
+  }
+  const float* bsrc[2] = {d->b_k, d->b_v};
+  for (int kv = 0; kv < 2; ++kv) {
+    if (bsrc[kv])
+      e = hipMemcpy(p->bias[kv], bsrc[kv], bbytes, hipMemcpyDeviceToDevice);
+    else
+      e = hipMemset(p->bias[kv], 0, bbytes);
+    if (e != hipSuccess) return fail(hip_fail(e));
+  }
+  e = hipMemcpy(p->layer_map, d->layer_map, mbytes, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail(hip_fail(e));
+  std::vector<double> fsv = rope_table(d->src), ftv = rope_table(d->tgt);
+  e = hipMemcpy(p->fs, fsv.data(), fsb, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail(hip_fail(e));
+  e = hipMemcpy(p->ft, ftv.data(), ftb, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail(hip_fail(e));
+  e = hipDeviceSynchronize();
+  if (e != hipSuccess) return fail(hip_fail(e));
+  *out = p;
+  return KVX_OK;
+}
+
+void kvx_plan_destroy(kvx_plan* p) {
+  if (!p) return;
+  if (p->block) (void)hipFree(p->block);
+  delete p;
+}
+
+kvx_status kvx_plan_query(const kvx_plan* p, kvx_plan_info* info) {
+  if (!p || !info) return KVX_EINVAL;
+  info->kernel = p->kernel;
+  info->tile_rows = p->kernel == kFused ? kMT : 0;
+  info->tile_cols = p->kernel == kFused ? kNT : 0;
+  info->threads = p->kernel == kFused ? kThreads : 256;
+  info->split_k = p->kernel == kFused && p->precision == KVX_PREC_BF16X2;
+  info->weight_bytes = p->bytes;
+  return KVX_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+int tiled_rows(int din) {
+  int r = 16384 / (din > 0 ? din : 1);
+  return r < 1 ? 1 : (r > 16 ? 16 : r);
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// Host-side check of device CSR contents (validation mode only).
+kvx_status validate_csr(const kvx_io& io, int64_t rows, hipStream_t st) {
+  std::vector<int32_t> rp(rows + 1);
+  hipError_t e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e);
+  e = hipMemcpy(rp.data(), io.row_ptr, (rows + 1) * sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  if (rp[0] != 0) return KVX_EDATA;
+  for (int64_t r = 0; r < rows; ++r)
+    if (rp[r + 1] < rp[r]) return KVX_EDATA;
+  const int64_t nnz = rp[rows];
+  std::vector<int32_t> ci(nnz > 0 ? nnz : 1);
+  if (nnz > 0) {
+    e = hipMemcpy(ci.data(), io.col_idx, nnz * sizeof(int32_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  for (int64_t i = 0; i < nnz; ++i)
+    if (ci[i] < 0 || ci[i] >= io.src_tokens) return KVX_EDATA;
+  return KVX_OK;
+}
+
+}  // namespace
+
+extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void* stream) {
+  if (!p || !io_in) return KVX_EINVAL;
+  kvx_io io = *io_in;
+  if (io.batch < 0 || io.src_tokens < 0 || io.tgt_capacity < 0) return KVX_EINVAL;
+  if (io.batch == 0) return KVX_OK;
+  const bool identity = io.tgt_tokens == nullptr;
+  std::vector<int32_t> ttok(io.batch);
+  int64_t rows = 0;
+  for (int b = 0; b < io.batch; ++b) {
+    const int32_t t = identity ? io.src_tokens : io.tgt_tokens[b];
+    if (t < 0) return KVX_EINVAL;
+    if (t > io.tgt_capacity) return KVX_ESHAPE;
+    ttok[b] = t;
+    rows += t;
+  }
+  if (rows == 0) return KVX_OK;
+  if (!io.src_k || !io.src_v || !io.tgt_k || !io.tgt_v) return KVX_EINVAL;
+  if (!identity && (!io.row_ptr || !io.col_idx || !io.weight)) return KVX_EINVAL;
+  if (rows > INT32_MAX / 2) return KVX_ESHAPE;
+
+  const int64_t Ls = p->src.n_layers, Hs = p->src.n_kv_heads, Ds = p->src.head_dim;
+  const int64_t Lt = p->tgt.n_layers, Ht = p->tgt.n_kv_heads, Dt = p->tgt.head_dim;
+  const int64_t B = io.batch;
+  auto all_zero = [](const int64_t* s) { return !s[0] && !s[1] && !s[2] && !s[3]; };
+  if (all_zero(io.src_stride)) {
+    io.src_stride[3] = Ds;
+    io.src_stride[2] = Ds * io.src_tokens;
+    io.src_stride[1] = Hs * io.src_stride[2];
+    io.src_stride[0] = B * io.src_stride[1];
+  }
+  if (all_zero(io.tgt_stride)) {
+    io.tgt_stride[3] = Dt;
+    io.tgt_stride[2] = Dt * int64_t(io.tgt_capacity);
+    io.tgt_stride[1] = Ht * io.tgt_stride[2];
+    io.tgt_stride[0] = B * io.tgt_stride[1];
+  }
+  for (int i = 0; i < 4; ++i)
+    if (io.src_stride[i] < 0 || io.tgt_stride[i] < 0) return KVX_ESHAPE;
+  // strides must keep one row (head_dim values) inside the next-outer step
+  if ((io.src_stride[3] < Ds && io.src_tokens > 1) || (io.tgt_stride[3] < Dt && io.tgt_capacity > 1))
+    return KVX_ESHAPE;
+  (void)Ls;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const char* vmode = std::getenv("KVX_VALIDATE");
+  if (!identity && vmode && vmode[0] == '1') {
+    kvx_status s = validate_csr(io, rows, st);
+    if (s != KVX_OK) return s;
+  }
+
+  const int esz = p->dtype == KVX_F32 ? 4 : 2;
+  bool fused = p->kernel == kFused;
+  if (fused) {
+    // 16-byte vector access needs 16-byte aligned rows
+    for (int i = 0; i < 4; ++i)
+      if ((io.src_stride[i] * esz) % 16 || (io.tgt_stride[i] * esz) % 16) fused = false;
+    if (!aligned16(io.src_k) || !aligned16(io.src_v) || !aligned16(io.tgt_k) ||
+        !aligned16(io.tgt_v))
+      fused = false;
+  }
+  if (p->kernel == kFused && !fused) return KVX_EUNSUPPORTED;
+
+  const Strides ss{io.src_stride[0], io.src_stride[1], io.src_stride[2], io.src_stride[3]};
+  const Strides ts{io.tgt_stride[0], io.tgt_stride[1], io.tgt_stride[2], io.tgt_stride[3]};
+  int64_t row_base = 0;
+  for (int64_t b0 = 0; b0 < B; b0 += kMaxBatch) {
+    const int nb = static_cast<int>(B - b0 < kMaxBatch ? B - b0 : kMaxBatch);
+    BatchArgs ba{};
+    ba.n = nb;
+    const int rows_per_tile = fused ? kMT : tiled_rows(p->din);
+    int tiles = 0;
+    for (int i = 0; i < nb; ++i) {
+      ba.tile_start[i] = tiles;
+      ba.t_tgt[i] = ttok[b0 + i];
+      ba.row_base[i] = static_cast<int32_t>(row_base);
+      row_base += ttok[b0 + i];
+      tiles += (ttok[b0 + i] + rows_per_tile - 1) / rows_per_tile;
+    }
+    ba.tile_start[nb] = tiles;
+    if (tiles == 0) continue;
+    const char* sk = static_cast<const char*>(io.src_k) + b0 * io.src_stride[1] * esz;
+    const char* sv = static_cast<const char*>(io.src_v) + b0 * io.src_stride[1] * esz;
+    char* tk = static_cast<char*>(io.tgt_k) + b0 * io.tgt_stride[1] * esz;
+    char* tv = static_cast<char*>(io.tgt_v) + b0 * io.tgt_stride[1] * esz;
+    if (fused) {
+      FusedArgs a{};
+      a.src[0] = reinterpret_cast<const bf16_t*>(sk);
+      a.src[1] = reinterpret_cast<const bf16_t*>(sv);
+      a.ss = ss;
+      a.tgt[0] = reinterpret_cast<bf16_t*>(tk);
+      a.tgt[1] = reinterpret_cast<bf16_t*>(tv);
+      a.ts = ts;
+      a.wp[0] = static_cast<const bf16x8*>(p->w[0]);
+      a.wp[1] = static_cast<const bf16x8*>(p->w[1]);
+      a.bias[0] = p->bias[0];
+      a.bias[1] = p->bias[1];
+      a.layer_map = p->layer_map;
+      a.mix = p->mix;
+      a.hs = static_cast<int32_t>(Hs);
+      a.ht = static_cast<int32_t>(Ht);
+      a.dt = static_cast<int32_t>(Dt);
+      a.din = p->din;
+      a.dout = p->dout;
+      a.fs = p->fs;
+      a.ft = p->ft;
+      a.row_ptr = io.row_ptr;
+      a.col_idx = io.col_idx;
+      a.weight = io.weight;
+      a.identity = identity;
+      a.split_k = p->precision == KVX_PREC_BF16X2;
+      a.split_v = p->precision == KVX_PREC_BF16X2 && !identity;
+      a.n_tiles = (p->dout / 64 + 3) / 4;
+      a.row_tiles = tiles;
+      a.ba = ba;
+      const int64_t grid = int64_t(tiles) * a.n_tiles * 2 * Lt;
+      if (grid > INT32_MAX) return KVX_ESHAPE;
+      switch (Ds) {
+        case 64: fused_kernel<64><<<dim3(grid), dim3(kThreads), 0, st>>>(a); break;
+        case 128: fused_kernel<128><<<dim3(grid), dim3(kThreads), 0, st>>>(a); break;
+        case 256: fused_kernel<256><<<dim3(grid), dim3(kThreads), 0, st>>>(a); break;
+        default: return KVX_EUNSUPPORTED;
+      }
+    } else {
+      const size_t lds = size_t(rows_per_tile) * p->din * sizeof(float);
+      if (p->dtype == KVX_F32) {
+        TiledArgs<float> a{};
+        a.src[0] = reinterpret_cast<const float*>(sk);
+        a.src[1] = reinterpret_cast<const float*>(sv);
+        a.tgt[0] = reinterpret_cast<float*>(tk);
+        a.tgt[1] = reinterpret_cast<float*>(tv);
+        a.w[0] = static_cast<const float*>(p->w[0]);
+        a.w[1] = static_cast<const float*>(p->w[1]);
+        a.ss = ss; a.ts = ts;
+        a.bias[0] = p->bias[0]; a.bias[1] = p->bias[1];
+        a.layer_map = p->layer_map; a.mix = p->mix;
+        a.hs = Hs; a.ds = Ds; a.ht = Ht; a.dt = Dt; a.din = p->din; a.dout = p->dout;
+        a.fs = p->fs; a.ft = p->ft;
+        a.row_ptr = io.row_ptr; a.col_idx = io.col_idx; a.weight = io.weight;
+        a.identity = identity; a.rows = rows_per_tile; a.ba = ba;
+        tiled_kernel<float><<<dim3(tiles, Lt, 2), dim3(256), lds, st>>>(a);
+      } else {
+        TiledArgs<bf16_t> a{};
+        a.src[0] = reinterpret_cast<const bf16_t*>(sk);
+        a.src[1] = reinterpret_cast<const bf16_t*>(sv);
+        a.tgt[0] = reinterpret_cast<bf16_t*>(tk);
+        a.tgt[1] = reinterpret_cast<bf16_t*>(tv);
+        a.w[0] = static_cast<const bf16_t*>(p->w[0]);
+        a.w[1] = static_cast<const bf16_t*>(p->w[1]);
+        a.ss = ss; a.ts = ts;
+        a.bias[0] = p->bias[0]; a.bias[1] = p->bias[1];
+        a.layer_map = p->layer_map; a.mix = p->mix;
+        a.hs = Hs; a.ds = Ds; a.ht = Ht; a.dt = Dt; a.din = p->din; a.dout = p->dout;
+        a.fs = p->fs; a.ft = p->ft;
+        a.row_ptr = io.row_ptr; a.col_idx = io.col_idx; a.weight = io.weight;
+        a.identity = identity; a.rows = rows_per_tile; a.ba = ba;
+        tiled_kernel<bf16_t><<<dim3(tiles, Lt, 2), dim3(256), lds, st>>>(a);
+      }
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  return KVX_OK;
+}

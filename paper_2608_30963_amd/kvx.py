@@ -1,0 +1,224 @@
+"""Python binding of ``libkvx.so`` (argument marshalling only).
+
+The three entry points carry the C names -- ``kvx_plan_create``,
+``kvx_translate``, ``kvx_plan_destroy`` -- and take torch tensors for device
+buffers (torch provides device memory and streams; it computes nothing here).
+Every step of the translation runs in the library's HIP kernels.
+
+The library must have been built (``python -m paper_2608_30963_amd.build``);
+loading fails loudly otherwise -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkvx.so")
+
+KVX_OK, KVX_EINVAL, KVX_ESHAPE, KVX_EUNSUPPORTED, KVX_ENOMEM, KVX_EHIP, KVX_EDATA = range(7)
+KVX_F32, KVX_BF16 = 0, 1
+KVX_PREC_BF16X2, KVX_PREC_BF16 = 0, 1
+
+# Exported C symbols, as declared in include/kvx.h.
+SYMBOLS = ("kvx_plan_create", "kvx_translate", "kvx_plan_destroy", "kvx_status_string",
+           "kvx_last_hip_error", "kvx_plan_query")
+
+
+class KvxError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+class Model(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("rope_base", C.c_double), ("inv_freq", C.c_void_p)]
+
+
+class PlanDesc(C.Structure):
+    _fields_ = [("src", Model), ("tgt", Model), ("mix", C.c_int32),
+                ("layer_map", C.c_void_p), ("dtype", C.c_int32),
+                ("w_k", C.c_void_p), ("w_v", C.c_void_p),
+                ("b_k", C.c_void_p), ("b_v", C.c_void_p), ("precision", C.c_int32)]
+
+
+class IO(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("src_tokens", C.c_int32),
+                ("src_k", C.c_void_p), ("src_v", C.c_void_p), ("src_stride", C.c_int64 * 4),
+                ("tgt_tokens", C.c_void_p), ("row_ptr", C.c_void_p),
+                ("col_idx", C.c_void_p), ("weight", C.c_void_p),
+                ("tgt_k", C.c_void_p), ("tgt_v", C.c_void_p), ("tgt_stride", C.c_int64 * 4),
+                ("tgt_capacity", C.c_int32)]
+
+
+class PlanInfo(C.Structure):
+    _fields_ = [("kernel", C.c_int32), ("tile_rows", C.c_int32), ("tile_cols", C.c_int32),
+                ("threads", C.c_int32), ("split_k", C.c_int32), ("weight_bytes", C.c_int64)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libkvx.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2608_30963_amd.build` (no fallback exists)")
+    lib = C.CDLL(path)
+    lib.kvx_plan_create.argtypes = [C.POINTER(PlanDesc), C.POINTER(C.c_void_p)]
+    lib.kvx_plan_create.restype = C.c_int
+    lib.kvx_translate.argtypes = [C.c_void_p, C.POINTER(IO), C.c_void_p]
+    lib.kvx_translate.restype = C.c_int
+    lib.kvx_plan_destroy.argtypes = [C.c_void_p]
+    lib.kvx_plan_destroy.restype = None
+    lib.kvx_status_string.argtypes = [C.c_int]
+    lib.kvx_status_string.restype = C.c_char_p
+    lib.kvx_last_hip_error.restype = C.c_int32
+    lib.kvx_plan_query.argtypes = [C.c_void_p, C.POINTER(PlanInfo)]
+    lib.kvx_plan_query.restype = C.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().kvx_status_string(int(status)).decode()
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if hasattr(t, "data_ptr"):
+        return t.data_ptr()
+    return int(t)
+
+
+def _host_array(values, ctype):
+    if values is None:
+        return None
+    vals = list(values)
+    return (ctype * max(1, len(vals)))(*vals)
+
+
+@dataclass
+class ModelShape:
+    n_layers: int
+    n_kv_heads: int
+    head_dim: int
+    rope_base: float
+
+
+def _model(m, inv_freq, keep) -> Model:
+    inv = None
+    if inv_freq is not None:
+        inv = _host_array([float(x) for x in inv_freq], C.c_double)
+        keep.append(inv)
+    return Model(int(m.n_layers), int(m.n_kv_heads), int(m.head_dim), float(m.rope_base),
+                 C.cast(inv, C.c_void_p).value if inv is not None else None)
+
+
+def kvx_plan_create(src, tgt, mix: int, layer_map: Sequence[int], dtype: int, w_k, w_v,
+                    b_k=None, b_v=None, precision: int = KVX_PREC_BF16X2,
+                    src_inv_freq=None, tgt_inv_freq=None) -> int:
+    """Create a plan; returns the opaque handle (an int).  ``w_k``/``w_v``/
+    ``b_k``/``b_v`` are device tensors (or raw device pointers)."""
+    lib = load()
+    keep = []
+    lm = _host_array([int(x) for x in layer_map], C.c_int32)
+    keep.append(lm)
+    desc = PlanDesc(_model(src, src_inv_freq, keep), _model(tgt, tgt_inv_freq, keep),
+                    int(mix), C.cast(lm, C.c_void_p).value, int(dtype), _ptr(w_k), _ptr(w_v),
+                    _ptr(b_k), _ptr(b_v), int(precision))
+    h = C.c_void_p()
+    st = lib.kvx_plan_create(C.byref(desc), C.byref(h))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_plan_create")
+    return h.value
+
+
+def make_io(batch: int, src_tokens: int, src_k, src_v, tgt_k, tgt_v, tgt_capacity: int,
+            tgt_tokens=None, row_ptr=None, col_idx=None, weight=None,
+            src_stride=(0, 0, 0, 0), tgt_stride=(0, 0, 0, 0)):
+    """Build the kvx_io struct; returns (io, keepalive)."""
+    keep = []
+    tt = None
+    if tgt_tokens is not None:
+        tt = _host_array([int(x) for x in tgt_tokens], C.c_int32)
+        keep.append(tt)
+    io = IO(int(batch), int(src_tokens), _ptr(src_k), _ptr(src_v),
+            (C.c_int64 * 4)(*[int(x) for x in src_stride]),
+            C.cast(tt, C.c_void_p).value if tt is not None else None,
+            _ptr(row_ptr), _ptr(col_idx), _ptr(weight), _ptr(tgt_k), _ptr(tgt_v),
+            (C.c_int64 * 4)(*[int(x) for x in tgt_stride]), int(tgt_capacity))
+    return io, keep
+
+
+def kvx_translate(plan: int, io: IO, stream=None) -> int:
+    """Enqueue a translation; ``stream`` is a torch stream, a raw hipStream_t
+    (int) or None (the current torch stream)."""
+    lib = load()
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    st = lib.kvx_translate(C.c_void_p(plan), C.byref(io), C.c_void_p(handle))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_translate")
+    return st
+
+
+def kvx_translate_status(plan, io: IO, stream_handle: int = 0) -> int:
+    """Raw status of kvx_translate (no exception)."""
+    return int(load().kvx_translate(C.c_void_p(plan), C.byref(io), C.c_void_p(stream_handle)))
+
+
+def kvx_plan_destroy(plan: Optional[int]) -> None:
+    load().kvx_plan_destroy(C.c_void_p(plan) if plan else None)
+
+
+def kvx_plan_query(plan: int) -> PlanInfo:
+    info = PlanInfo()
+    st = load().kvx_plan_query(C.c_void_p(plan), C.byref(info))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_plan_query")
+    return info
+
+
+class Translator:
+    """RAII wrapper around a plan, for the tests and the benchmark."""
+
+    def __init__(self, src, tgt, mix, layer_map, dtype, w_k, w_v, b_k=None, b_v=None,
+                 precision=KVX_PREC_BF16X2, src_inv_freq=None, tgt_inv_freq=None):
+        self.src, self.tgt, self.mix = src, tgt, mix
+        self.dtype = dtype
+        self.plan = kvx_plan_create(src, tgt, mix, layer_map, dtype, w_k, w_v, b_k, b_v,
+                                    precision, src_inv_freq, tgt_inv_freq)
+
+    def info(self) -> PlanInfo:
+        return kvx_plan_query(self.plan)
+
+    def __call__(self, src_k, src_v, tgt_k, tgt_v, tgt_capacity=None, tgt_tokens=None,
+                 row_ptr=None, col_idx=None, weight=None, stream=None,
+                 src_stride=(0, 0, 0, 0), tgt_stride=(0, 0, 0, 0)):
+        batch, src_tokens = int(src_k.shape[1]), int(src_k.shape[3])
+        cap = int(tgt_k.shape[3]) if tgt_capacity is None else int(tgt_capacity)
+        io, keep = make_io(batch, src_tokens, src_k, src_v, tgt_k, tgt_v, cap, tgt_tokens,
+                           row_ptr, col_idx, weight, src_stride, tgt_stride)
+        kvx_translate(self.plan, io, stream)
+        del keep
+
+    def close(self):
+        if self.plan:
+            kvx_plan_destroy(self.plan)
+            self.plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

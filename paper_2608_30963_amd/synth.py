@@ -168,11 +168,15 @@ def config(cfg_id: int, src_tokens: Optional[int] = None, batch: Optional[int] =
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round-to-nearest-even float32 -> bfloat16, returned as uint16 bits."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32)
     if np.isnan(x).any():
         raise ValueError("NaN in synthetic input")
-    bias = ((u >> 16) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + bias) >> 16).astype(np.uint16)
+    u = x.view(np.uint32)
+    t = u >> np.uint32(16)
+    t &= np.uint32(1)
+    t += np.uint32(0x7FFF)
+    t += u
+    t >>= np.uint32(16)
+    return t.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:

@@ -1,0 +1,109 @@
+"""Helpers of the GPU tests: upload a problem, run the library, compare with
+the oracle.
+
+Tolerances (translated K/V against the fp64 oracle, per tensor = one target
+layer's K or V):
+* bf16: element-wise |g - r| <= 2e-2 * max(1, |r|) and relative Frobenius
+  error <= 1e-2.  The literal max-abs bound cannot hold for bf16 outputs above
+  |r| = 8 (half an ulp there is 2^-5 > 2e-2), so it scales with |r| beyond 1.
+* fp32: the same form with 1e-5.
+Integer work (layer map, alignment, head/token indexing) is checked bit-exact
+by the probe tests.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from paper_2608_30963_amd import kvx, synth as S
+
+TOL = {S.BF16: (2e-2, 1e-2), S.F32: (1e-5, 1e-5)}
+
+
+def torch():
+    import torch as _t
+    return _t
+
+
+def np_to_dev(a: np.ndarray, dtype: str):
+    T = torch()
+    if a is None:
+        return None
+    if dtype == S.BF16 and a.dtype == np.uint16:
+        return T.from_numpy(a.view(np.int16).copy()).view(T.bfloat16).cuda()
+    return T.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def dev_to_f64(t, dtype: str) -> np.ndarray:
+    T = torch()
+    if t.dtype == T.bfloat16:
+        return t.float().cpu().numpy().astype(np.float64)
+    return t.cpu().numpy().astype(np.float64)
+
+
+class DevProblem:
+    """Device copies of a problem's arrays plus a plan."""
+
+    def __init__(self, prob: S.Problem, precision=kvx.KVX_PREC_BF16X2, cap=None, fill=None):
+        T = torch()
+        spec = prob.spec
+        self.prob = prob
+        self.spec = spec
+        dt = spec.dtype
+        self.kdtype = kvx.KVX_BF16 if dt == S.BF16 else kvx.KVX_F32
+        self.src_k = np_to_dev(prob.src_k, dt)
+        self.src_v = np_to_dev(prob.src_v, dt)
+        self.w_k = np_to_dev(prob.w_k, dt)
+        self.w_v = np_to_dev(prob.w_v, dt)
+        self.b_k = np_to_dev(prob.b_k, S.F32)
+        self.b_v = np_to_dev(prob.b_v, S.F32)
+        self.row_ptr = np_to_dev(prob.row_ptr, S.F32) if prob.row_ptr is not None else None
+        self.col_idx = np_to_dev(prob.col_idx, S.F32) if prob.col_idx is not None else None
+        self.weight = np_to_dev(prob.weight, S.F32) if prob.weight is not None else None
+        self.tr = kvx.Translator(spec.src, spec.tgt, spec.mix, spec.layer_map, self.kdtype,
+                                 self.w_k, self.w_v, self.b_k, self.b_v, precision)
+        self.cap = prob.tgt_capacity if cap is None else cap
+        shape = (spec.tgt.n_layers, spec.batch, spec.tgt.n_kv_heads, self.cap,
+                 spec.tgt.head_dim)
+        tdt = T.bfloat16 if dt == S.BF16 else T.float32
+        fill = float("nan") if fill is None else fill
+        self.tgt_k = T.full(shape, fill, dtype=tdt, device="cuda")
+        self.tgt_v = T.full(shape, fill, dtype=tdt, device="cuda")
+
+    def run(self, stream=None):
+        ident = self.prob.row_ptr is None
+        self.tr(self.src_k, self.src_v, self.tgt_k, self.tgt_v, self.cap,
+                None if ident else self.prob.tgt_tokens,
+                self.row_ptr, self.col_idx, self.weight, stream=stream)
+        return self.tgt_k, self.tgt_v
+
+    def close(self):
+        self.tr.close()
+
+
+def check_close(got: np.ndarray, ref: np.ndarray, dtype: str, what: str):
+    """Element-wise and relative-Frobenius check; returns the metrics."""
+    el, fro = TOL[dtype]
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    d = np.abs(got - ref)
+    scaled = d / np.maximum(1.0, np.abs(ref))
+    worst = float(scaled.max()) if d.size else 0.0
+    rf = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300)) if d.size else 0.0
+    assert worst <= el, f"{what}: element error {worst:.3e} > {el} (max abs {d.max():.3e})"
+    assert rf <= fro, f"{what}: relative Frobenius {rf:.3e} > {fro}"
+    return {"max_scaled": worst, "max_abs": float(d.max()) if d.size else 0.0, "rel_fro": rf}
+
+
+def check_full(dev: DevProblem, ref_k: np.ndarray, ref_v: np.ndarray, what: str):
+    """Compare every valid row of every target layer against the oracle."""
+    spec = dev.spec
+    gk = dev_to_f64(dev.tgt_k, spec.dtype)
+    gv = dev_to_f64(dev.tgt_v, spec.dtype)
+    out = []
+    tt = dev.prob.tgt_tokens
+    for l in range(spec.tgt.n_layers):
+        for name, g, r in (("K", gk, ref_k), ("V", gv, ref_v)):
+            gs = np.concatenate([g[l, b, :, :tt[b]].reshape(-1) for b in range(spec.batch)])
+            rs = np.concatenate([r[l, b, :, :tt[b]].reshape(-1) for b in range(spec.batch)])
+            out.append(check_close(gs, rs, spec.dtype, f"{what} layer {l} {name}"))
+    return out

@@ -1,0 +1,108 @@
+"""The C-ABI library on the host: it loads, exports every symbol the header
+declares, and rejects invalid arguments before touching the device.
+No compute call is made here (no GPU needed)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2608_30963_amd import kvx
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "kvx.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(kvx_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = kvx.load()
+    names = _declared()
+    assert {"kvx_plan_create", "kvx_translate", "kvx_plan_destroy"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(kvx.SYMBOLS)
+
+
+def test_status_strings():
+    for s in range(7):
+        assert kvx.status_string(s)
+    assert kvx.status_string(0) == "ok"
+
+
+def _desc(**kw):
+    src = kvx.Model(4, 2, 64, 1e4, None)
+    tgt = kvx.Model(4, 2, 64, 1e4, None)
+    lm = (C.c_int32 * 4)(0, 1, 2, 3)
+    base = dict(src=src, tgt=tgt, mix=1, layer_map=C.cast(lm, C.c_void_p).value,
+                dtype=kvx.KVX_BF16, w_k=0x1000, w_v=0x2000, b_k=None, b_v=None,
+                precision=kvx.KVX_PREC_BF16X2)
+    base.update(kw)
+    return kvx.PlanDesc(**base), lm
+
+
+def _create(desc):
+    h = C.c_void_p(12345)
+    st = kvx.load().kvx_plan_create(C.byref(desc), C.byref(h))
+    return st, h.value
+
+
+def test_plan_create_rejects_null():
+    lib = kvx.load()
+    assert lib.kvx_plan_create(None, None) == kvx.KVX_EINVAL
+    d, keep = _desc()
+    assert lib.kvx_plan_create(C.byref(d), None) == kvx.KVX_EINVAL
+    d, keep = _desc(w_k=None)
+    st, h = _create(d)
+    assert st == kvx.KVX_EINVAL and h is None
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("mix", 0, kvx.KVX_EINVAL),
+    ("dtype", 7, kvx.KVX_EINVAL),
+    ("precision", 9, kvx.KVX_EINVAL),
+])
+def test_plan_create_rejects_bad_fields(field, value, status):
+    d, keep = _desc(**{field: value})
+    st, h = _create(d)
+    assert st == status and h is None
+
+
+def test_plan_create_rejects_bad_models():
+    d, keep = _desc(src=kvx.Model(4, 2, 63, 1e4, None))
+    assert _create(d)[0] == kvx.KVX_EUNSUPPORTED
+    d, keep = _desc(tgt=kvx.Model(0, 2, 64, 1e4, None))
+    assert _create(d)[0] == kvx.KVX_EINVAL
+    d, keep = _desc(src=kvx.Model(4, 2, 64, float("nan"), None))
+    assert _create(d)[0] == kvx.KVX_EINVAL
+
+
+def test_plan_create_rejects_layer_map_out_of_range():
+    lm = (C.c_int32 * 4)(0, 1, 2, 4)
+    d, keep = _desc(layer_map=C.cast(lm, C.c_void_p).value)
+    assert _create(d)[0] == kvx.KVX_EINVAL
+    lm2 = (C.c_int32 * 4)(0, -1, 2, 3)
+    d, keep = _desc(layer_map=C.cast(lm2, C.c_void_p).value)
+    assert _create(d)[0] == kvx.KVX_EINVAL
+
+
+def test_plan_create_rejects_bad_inv_freq():
+    inv = (C.c_double * 32)(*([float("inf")] * 32))
+    d, keep = _desc(src=kvx.Model(4, 2, 64, 1e4, C.cast(inv, C.c_void_p).value))
+    assert _create(d)[0] == kvx.KVX_EINVAL
+
+
+def test_translate_rejects_null_and_destroy_is_null_safe():
+    lib = kvx.load()
+    io, keep = kvx.make_io(1, 4, 0x10, 0x10, 0x10, 0x10, 4)
+    assert lib.kvx_translate(None, C.byref(io), None) == kvx.KVX_EINVAL
+    assert lib.kvx_translate(C.c_void_p(1), None, None) == kvx.KVX_EINVAL
+    kvx.kvx_plan_destroy(None)
+
+
+def test_query_rejects_null():
+    info = kvx.PlanInfo()
+    assert kvx.load().kvx_plan_query(None, C.byref(info)) == kvx.KVX_EINVAL

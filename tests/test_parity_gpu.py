@@ -1,0 +1,114 @@
+"""GPU parity: the HIP path (through the C-ABI) against the fp64 oracle.
+
+Small cases (a few tiles plus a ragged tail) are compared on every output
+element; the full-size workloads are compared on sampled rows the oracle
+computes one by one (first and last rows of tiles, context edges, random
+rows) in the same launch configuration the benchmark times.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2608_30963_amd import kvx, synth as S
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+
+def _full(spec, precision=kvx.KVX_PREC_BF16X2, expect_kernel=None):
+    prob = S.make_problem(spec)
+    print(f"[parity] {spec.name} T={spec.src_tokens} B={spec.batch}", flush=True)
+    dev = U.DevProblem(prob, precision)
+    if expect_kernel is not None:
+        assert dev.tr.info().kernel == expect_kernel
+    dev.run()
+    U.torch().cuda.synchronize()
+    rk, rv = O.translate(prob)
+    m = U.check_full(dev, rk, rv, spec.name)
+    dev.close()
+    return m
+
+
+def test_config1_fp32_full():
+    _full(S.config(1), expect_kernel=0)
+
+
+def test_config1_fp32_ragged_tail():
+    _full(S.config(1, src_tokens=100, batch=3), expect_kernel=0)
+
+
+def test_config2_small_ragged():
+    _full(S.config(2, src_tokens=300), expect_kernel=1)
+
+
+def test_config3_small_ragged():
+    _full(S.config(3, src_tokens=700, batch=2), expect_kernel=1)
+
+
+def test_config4_1k_batch8():
+    _full(S.config(4, src_tokens=1024), expect_kernel=1)
+
+
+def test_config5_small():
+    _full(S.config(5, src_tokens=384), expect_kernel=1)
+
+
+def test_config2_single_precision_mode_no_outliers():
+    # single bf16 rounding of the operand is within tolerance without outliers
+    _full(S.config(2, src_tokens=260).replace(outliers=0), precision=kvx.KVX_PREC_BF16)
+
+
+def _sample_rows(prob, n_layers_pick, rng):
+    spec = prob.spec
+    Lt = spec.tgt.n_layers
+    layers = sorted(set([0, Lt - 1] + list(rng.integers(0, Lt, n_layers_pick))))
+    L, B, T = [], [], []
+    for l in layers:
+        for b in range(spec.batch):
+            tt = int(prob.tgt_tokens[b])
+            cand = {0, tt - 1, min(127, tt - 1), min(128, tt - 1), tt // 2}
+            cand |= set(int(x) for x in rng.integers(0, tt, 24))
+            for t in sorted(cand):
+                L.append(l)
+                B.append(b)
+                T.append(t)
+    return np.array(L), np.array(B), np.array(T)
+
+
+def _sampled(spec, precision=kvx.KVX_PREC_BF16X2, n_layers_pick=3):
+    rng = np.random.default_rng(spec.cfg_id)
+    prob = S.make_problem(spec)
+    print(f"[parity-sampled] {spec.name} T={spec.src_tokens} B={spec.batch}", flush=True)
+    dev = U.DevProblem(prob, precision)
+    dev.run()
+    U.torch().cuda.synchronize()
+    L, B, T = _sample_rows(prob, n_layers_pick, rng)
+    rk, rv = O.rows(prob, L, B, T)
+    gk = U.dev_to_f64(dev.tgt_k, spec.dtype)
+    gv = U.dev_to_f64(dev.tgt_v, spec.dtype)
+    gk = gk[L, B, :, T, :].reshape(len(L), -1)
+    gv = gv[L, B, :, T, :].reshape(len(L), -1)
+    for l in np.unique(L):
+        sel = L == l
+        U.check_close(gk[sel], rk[sel], spec.dtype, f"{spec.name} layer {l} K")
+        U.check_close(gv[sel], rv[sel], spec.dtype, f"{spec.name} layer {l} V")
+    # every valid row was written (targets start as NaN)
+    for b in range(spec.batch):
+        tt = int(prob.tgt_tokens[b])
+        assert not U.torch().isnan(dev.tgt_k[:, b, :, :tt]).any()
+        assert not U.torch().isnan(dev.tgt_v[:, b, :, :tt]).any()
+        if tt < dev.cap:
+            assert U.torch().isnan(dev.tgt_k[:, b, :, tt:]).all()
+    dev.close()
+
+
+def test_config2_full_size_sampled():
+    _sampled(S.config(2))
+
+
+def test_config3_full_size_sampled():
+    _sampled(S.config(3))
+
+
+def test_config5_full_size_sampled():
+    _sampled(S.config(5), n_layers_pick=2)
