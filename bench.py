@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""Benchmark of the KV-translation operator on one MI355X.
+
+A step is one ``kvx_translate`` call: every target layer's K and V of one
+context, i.e. all stages of the translation (source-RoPE removal, alignment,
+projection, target RoPE, store into the target cache layout).  Plan creation
+(weight packing) happens once, before timing, as in serving.
+
+Default workload: Qwen2.5-7B -> Qwen2.5-1.5B shaped KV caches at a 4K-token
+context, bf16, same tokenizer (28 -> 28 layers, 4x128 -> 2x128 KV heads, RoPE
+base 1e6 on both sides, 4 outlier channels per head scaled x20), seeded
+synthetic data.  Inputs are resident in HBM before the timed region; three
+buffer sets rotate so no call finds its inputs in the 256 MB last-level cache.
+
+Prints one JSON line (rank 0).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 matrix peak, TFLOP/s
+METRIC = "translated tokens/s (all layers K+V) at 4K ctx; ms/handoff; % MFMA/HBM peak"
+
+
+def algorithmic(spec, prob):
+    """Bytes and flops the operator itself must move / compute per call:
+    each used source element read once, each target element written once,
+    translator weights read once, alignment map read once; flops of the
+    pooled-then-projected contraction."""
+    esz = 4 if spec.dtype == "f32" else 2
+    used = len(set(int(x) for x in spec.layer_map))
+    s = spec.src
+    rows = int(prob.tgt_tokens.sum())
+    read = 2 * used * spec.batch * s.n_kv_heads * spec.src_tokens * s.head_dim * esz
+    write = 2 * spec.tgt.n_layers * rows * spec.d_out * esz
+    weights = 2 * spec.tgt.n_layers * spec.d_out * spec.d_in * esz
+    amap = 0 if prob.row_ptr is None else prob.row_ptr.nbytes + prob.col_idx.nbytes + \
+        prob.weight.nbytes
+    flops = 2 * 2 * spec.tgt.n_layers * rows * spec.d_in * spec.d_out
+    return {"read": read, "write": write, "weights": weights, "map": amap,
+            "bytes": read + write + weights + amap, "flops": flops}
+
+
+def cpu_baseline(spec, prob, budget_s: float):
+    """Time the fp64 oracle on the host: all target layers of a bounded
+    number of tokens, scaled to source tokens per second."""
+    from oracle import oracle as O
+    lt = spec.tgt.n_layers
+    n_tok = 16
+    elapsed = 0.0
+    while True:
+        toks = np.linspace(0, int(prob.tgt_tokens[0]) - 1, n_tok).astype(np.int32)
+        L = np.repeat(np.arange(lt, dtype=np.int32), n_tok)
+        T = np.tile(toks, lt)
+        B = np.zeros_like(L)
+        t0 = time.perf_counter()
+        O.rows(prob, L, B, T)
+        elapsed = time.perf_counter() - t0
+        if elapsed >= budget_s or n_tok >= int(prob.tgt_tokens[0]):
+            break
+        n_tok = min(int(prob.tgt_tokens[0]), max(n_tok * 2, int(n_tok * budget_s / max(elapsed, 1e-3) * 1.1)))
+    # target rows per second -> source tokens per second (T_s / T_t source tokens per row)
+    src_per_row = spec.src_tokens * spec.batch / float(prob.tgt_tokens.sum())
+    return {"value": n_tok * src_per_row / elapsed, "unit": "tokens/s",
+            "cores": O.num_threads(), "kind": "oracle",
+            "sample": f"{n_tok} target tokens x all {lt} target layers (K and V), "
+                      f"fp64 C oracle, {elapsed:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, help="workload 1-5 (default 2)")
+    ap.add_argument("--tokens", type=int, default=None, help="override source tokens")
+    ap.add_argument("--batch", type=int, default=None, help="override contexts per call")
+    ap.add_argument("--sets", type=int, default=3, help="rotating buffer sets")
+    ap.add_argument("--precision", choices=["bf16x2", "bf16"], default="bf16x2")
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle time for the CPU baseline (0 = skip)")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="first run a plain device copy (bitwise_not) of this many MiB "
+                         "(three times), "
+                         "a known-size reference for the HBM byte counters")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs on one GPU only; the translation shards by "
+              "target layer with no exchange, but multi-GPU runs are not part of it "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_30963_amd import kvx, synth as S
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    kvx.load()  # fails loudly if the library is not built
+
+    spec = S.config(args.config, src_tokens=args.tokens, batch=args.batch)
+    print(f"[bench] generating {spec.name} T={spec.src_tokens} B={spec.batch}",
+          file=sys.stderr, flush=True)
+    prob = S.make_problem(spec)
+    alg = algorithmic(spec, prob)
+
+    def dev(a, f32=False):
+        if a is None:
+            return None
+        if spec.dtype == "bf16" and a.dtype == np.uint16 and not f32:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    kd = kvx.KVX_BF16 if spec.dtype == "bf16" else kvx.KVX_F32
+    prec = kvx.KVX_PREC_BF16X2 if args.precision == "bf16x2" else kvx.KVX_PREC_BF16
+    w_k, w_v = dev(prob.w_k), dev(prob.w_v)
+    tr = kvx.Translator(spec.src, spec.tgt, spec.mix, spec.layer_map, kd, w_k, w_v,
+                        dev(prob.b_k), dev(prob.b_v), prec)
+    del w_k, w_v
+    info = tr.info()
+    ident = prob.row_ptr is None
+    rp, ci, wt = (None, None, None) if ident else (dev(prob.row_ptr), dev(prob.col_idx),
+                                                  dev(prob.weight))
+    cap = prob.tgt_capacity
+    tdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
+    oshape = (spec.tgt.n_layers, spec.batch, spec.tgt.n_kv_heads, cap, spec.tgt.head_dim)
+    sk0, sv0 = dev(prob.src_k), dev(prob.src_v)
+    sets = []
+    for i in range(max(1, args.sets)):
+        sk = sk0 if i == 0 else sk0.clone()
+        sv = sv0 if i == 0 else sv0.clone()
+        tk = torch.empty(oshape, dtype=tdt, device="cuda")
+        tv = torch.empty(oshape, dtype=tdt, device="cuda")
+        sets.append((sk, sv, tk, tv))
+    tt = None if ident else prob.tgt_tokens
+    stream = torch.cuda.current_stream()
+    ios = [kvx.make_io(spec.batch, spec.src_tokens, s[0], s[1], s[2], s[3], cap, tt, rp, ci,
+                       wt) for s in sets]
+
+    def step(i):
+        kvx.kvx_translate(tr.plan, ios[i % len(ios)][0], stream)
+
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib << 20
+        csrc = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        cdst = torch.empty_like(csrc)
+        torch.cuda.synchronize()
+        for _ in range(3):  # an elementwise kernel: reads n bytes, writes n bytes
+            torch.bitwise_not(csrc, out=cdst)
+        torch.cuda.synchronize()
+        del csrc, cdst
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} calls); timing {args.steps}", file=sys.stderr,
+          flush=True)
+
+    # events on the stream the kernel is launched on bracket the timed calls
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall0
+    ms_ev = ev0.elapsed_time(ev1) / args.steps
+    ms_wall = t_wall * 1e3 / args.steps
+    ms = max(ms_ev, 0.0)
+
+    # one more call per set, checked for unwritten rows (targets start uninitialised,
+    # so fill with NaN first)
+    for s in sets:
+        s[2].fill_(float("nan"))
+        s[3].fill_(float("nan"))
+    for i in range(len(sets)):
+        step(i)
+    torch.cuda.synchronize()
+    for b in range(spec.batch):
+        t_b = int(prob.tgt_tokens[b])
+        for s in sets:
+            if torch.isnan(s[2][:, b, :, :t_b]).any() or torch.isnan(s[3][:, b, :, :t_b]).any():
+                print("bench.py: output has unwritten rows", file=sys.stderr)
+                sys.exit(1)
+
+    tokens = spec.batch * spec.src_tokens
+    value = tokens / (ms * 1e-3)
+    gbs = alg["bytes"] / (ms * 1e-3) / 1e9
+    tfs = alg["flops"] / (ms * 1e-3) / 1e12
+    kernel_name = "fused_kernel" if info.kernel == 1 else "tiled_kernel"
+    roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": kernel_name,
+            "bytes_per_launch": alg["bytes"], "mfma_tflops": round(tfs, 1),
+            "mfma_frac": round(tfs / MFMA_BF16_PEAK_TFS, 4)}
+
+    cpu = None
+    if not args.no_cpu and args.cpu_budget > 0:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(spec, prob, args.cpu_budget)
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": spec.dtype, "data": "synthetic",
+        "config": {"workload": spec.name, "src_tokens": spec.src_tokens,
+                   "tgt_tokens": int(prob.tgt_tokens.sum()), "batch": spec.batch,
+                   "src_layers": spec.src.n_layers, "tgt_layers": spec.tgt.n_layers,
+                   "src_heads": f"{spec.src.n_kv_heads}x{spec.src.head_dim}",
+                   "tgt_heads": f"{spec.tgt.n_kv_heads}x{spec.tgt.head_dim}",
+                   "mix": spec.mix, "precision": args.precision,
+                   "parallelism": "single GPU"},
+        "ms_per_handoff": round(ms, 5) if spec.batch == 1 else None,
+        "ms_wall_per_step": round(ms_wall, 5),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    tr.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -75,9 +75,20 @@ std::vector<double> rope_table(const kvx_model& m) {
 }
 
 bool fused_supported(const kvx_plan& p) {
-  const int ds = p.src.head_dim;
-  return p.dtype == KVX_BF16 && (ds == 64 || ds == 128 || ds == 256) &&
-         p.tgt.head_dim % 64 == 0 && p.dout % 64 == 0 && p.din % 16 == 0;
+  return p.dtype == KVX_BF16 && p.src.head_dim % 16 == 0 && p.din % 128 == 0 &&
+         p.tgt.head_dim % 64 == 0 && p.dout % 64 == 0;
+}
+
+// Input feature held in K-slot `k` of the fused kernel: chunk c = k / 128 holds
+// the RoPE pairs 64c .. 64c+63 of the flattened (mixed layer, head, d < Ds/2)
+// list, first members in slots 0..63, second members (d + Ds/2) in 64..127.
+int64_t fused_feature_of_slot(int64_t k, int64_t ds) {
+  const int64_t c = k / 128, s = k % 128;
+  const int64_t pair = 64 * c + (s % 64);
+  const int64_t half = ds / 2;
+  const int64_t head = pair / half;  // (j * Hs + h)
+  const int64_t d = pair % half + (s >= 64 ? half : 0);
+  return head * ds + d;
 }
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -172,19 +183,21 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
     if (e != hipSuccess) return fail(hip_fail(e));
     const void* up = host.data();
     if (p->kernel == kFused) {
-      // B fragment (n-block nb, k-step ks) of v_mfma_f32_32x32x16_bf16: lane
-      // holds W[nb*32 + lane%32][ks*16 + 8*(lane/32) + j], j < 8.
+      // A fragment (feature block nb, k-step ks) of v_mfma_f32_32x32x16_bf16:
+      // lane holds W[nb*32 + lane%32][feature of slot ks*16 + 8*(lane/32) + j].
       packed.resize(wbytes);
       const uint16_t* wsrc16 = reinterpret_cast<const uint16_t*>(host.data());
       uint16_t* dst = reinterpret_cast<uint16_t*>(packed.data());
       const int64_t nb_n = dout64 / 32, ks_n = din64 / 16;
+      std::vector<int64_t> feat(din64);
+      for (int64_t k = 0; k < din64; ++k) feat[k] = fused_feature_of_slot(k, d->src.head_dim);
       for (int64_t l = 0; l < lt; ++l)
         for (int64_t nb = 0; nb < nb_n; ++nb)
           for (int64_t ks = 0; ks < ks_n; ++ks)
             for (int lanei = 0; lanei < 64; ++lanei)
               for (int jj = 0; jj < 8; ++jj) {
                 const int64_t o = nb * 32 + lanei % 32;
-                const int64_t i = ks * 16 + 8 * (lanei / 32) + jj;
+                const int64_t i = feat[ks * 16 + 8 * (lanei / 32) + jj];
                 dst[((((l * nb_n + nb) * ks_n + ks) * 64 + lanei) * 8) + jj] =
                     wsrc16[(l * dout64 + o) * din64 + i];
               }
@@ -368,12 +381,12 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       a.dt = static_cast<int32_t>(Dt);
       a.din = p->din;
       a.dout = p->dout;
+      a.ds = static_cast<int32_t>(Ds);
       a.fs = p->fs;
       a.ft = p->ft;
       a.row_ptr = io.row_ptr;
       a.col_idx = io.col_idx;
       a.weight = io.weight;
-      a.identity = identity;
       a.split_k = p->precision == KVX_PREC_BF16X2;
       a.split_v = p->precision == KVX_PREC_BF16X2 && !identity;
       a.n_tiles = (p->dout / 64 + 3) / 4;
@@ -381,12 +394,10 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       a.ba = ba;
       const int64_t grid = int64_t(tiles) * a.n_tiles * 2 * Lt;
       if (grid > INT32_MAX) return KVX_ESHAPE;
-      switch (Ds) {
-        case 64: fused_kernel<64><<<dim3(grid), dim3(kThreads), 0, st>>>(a); break;
-        case 128: fused_kernel<128><<<dim3(grid), dim3(kThreads), 0, st>>>(a); break;
-        case 256: fused_kernel<256><<<dim3(grid), dim3(kThreads), 0, st>>>(a); break;
-        default: return KVX_EUNSUPPORTED;
-      }
+      if (identity)
+        fused_kernel<true><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+      else
+        fused_kernel<false><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
     } else {
       const size_t lds = size_t(rows_per_tile) * p->din * sizeof(float);
       if (p->dtype == KVX_F32) {
