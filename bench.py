@@ -86,7 +86,7 @@ def main():
     ap.add_argument("--tokens", type=int, default=None, help="override source tokens")
     ap.add_argument("--batch", type=int, default=None, help="override contexts per call")
     ap.add_argument("--sets", type=int, default=3, help="rotating buffer sets")
-    ap.add_argument("--precision", choices=["bf16x2", "bf16"], default="bf16x2")
+    ap.add_argument("--precision", choices=["bf16x2", "bf16", "f16"], default="bf16x2")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--no-cpu", action="store_true")
@@ -125,7 +125,8 @@ def main():
         return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
     kd = kvx.KVX_BF16 if spec.dtype == "bf16" else kvx.KVX_F32
-    prec = kvx.KVX_PREC_BF16X2 if args.precision == "bf16x2" else kvx.KVX_PREC_BF16
+    prec = {"bf16x2": kvx.KVX_PREC_BF16X2, "bf16": kvx.KVX_PREC_BF16,
+            "f16": kvx.KVX_PREC_F16}[args.precision]
     w_k, w_v = dev(prob.w_k), dev(prob.w_v)
     tr = kvx.Translator(spec.src, spec.tgt, spec.mix, spec.layer_map, kd, w_k, w_v,
                         dev(prob.b_k), dev(prob.b_v), prec)

@@ -48,13 +48,21 @@ typedef enum {
 typedef enum { KVX_F32 = 0, KVX_BF16 = 1 } kvx_dtype;
 
 /* Precision of the matrix-core operands (bf16 plans only; ignored for f32).
- *  KVX_PREC_BF16X2: a computed operand (RoPE-de-rotated K, pooled rows with
- *                   non-unit weights) is split a = hi + lo into two bf16
- *                   values and contracted twice against the same bf16 W;
- *                   operands that are already bf16 go through once.  Default.
- *  KVX_PREC_BF16:   every operand rounded once to bf16.
+ * A "computed" operand is one the translation produces before the projection:
+ * RoPE-de-rotated K, and pooled V rows when the tokenizers differ.  Source V
+ * with identity alignment is already bf16 and always goes through unchanged.
+ *  KVX_PREC_BF16X2: computed operands are split a = hi + lo into two bf16
+ *                   values and contracted twice against the bf16 W (relative
+ *                   operand error about 2^-17; no range limit).  Default.
+ *  KVX_PREC_BF16:   computed operands rounded once to bf16 (2^-9).
+ *  KVX_PREC_F16:    computed operands rounded once to fp16 and contracted
+ *                   against an fp16 copy of W (2^-12, one contraction).
+ *                   Range limit: a computed operand of magnitude >= 65520
+ *                   overflows and makes the affected outputs non-finite;
+ *                   kvx_plan_create returns KVX_EUNSUPPORTED if a weight
+ *                   exceeds the fp16 range.
  * Accumulation is fp32 in every mode. */
-typedef enum { KVX_PREC_BF16X2 = 0, KVX_PREC_BF16 = 1 } kvx_precision;
+typedef enum { KVX_PREC_BF16X2 = 0, KVX_PREC_BF16 = 1, KVX_PREC_F16 = 2 } kvx_precision;
 
 /* One side of the translation (a model's KV-cache geometry). */
 typedef struct {
@@ -139,7 +147,7 @@ typedef struct {
   int32_t tile_rows;     /* target rows per workgroup */
   int32_t tile_cols;     /* output features per workgroup */
   int32_t threads;       /* threads per workgroup */
-  int32_t split_k;       /* 1 when K operands are split hi/lo (BF16X2) */
+  int32_t precision;     /* kvx_precision of the plan */
   int64_t weight_bytes;  /* device bytes held by the plan */
 } kvx_plan_info;
 

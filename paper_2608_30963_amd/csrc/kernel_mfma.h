@@ -1,23 +1,25 @@
 // kernel_mfma.h -- fused bf16 translation kernel on the gfx950 matrix cores.
 //
-// One workgroup owns (target layer l, K|V, a tile of MT = 128 target rows of
-// one context, an N tile of 256 output features) and runs 8 waves in two
-// roles over a sequence of K-chunks:
+// Work unit ("tile"): (target layer l, K|V, 128 target rows of one context,
+// 256 output features).  The kernel is persistent: one workgroup per compute
+// unit walks a contiguous range of tiles (contiguous per XCD, so the weights
+// of a layer stay in that XCD's L2), and its 8 waves run in two roles over
+// the concatenated sequence of K-chunks of all its tiles:
 //
 //   producers (waves 0-3)  gather 16-byte pieces of the source rows named by
 //       the alignment entries of each target row, undo the source RoPE at
 //       each source position (fp64-reduced angle), pool with the entry
 //       weights in fp32, and write the chunk into one of two LDS buffers as
 //       bf16 -- as hi = bf16(z), lo = bf16(z - hi) when the operand is a
-//       computed value and the plan asks for the split.  Raw source data of
-//       the next chunk is prefetched into registers while the current one is
-//       transformed.
+//       computed value and the plan asks for the split.  Raw source data is
+//       prefetched a chunk ahead, across tile boundaries.
 //   consumers (waves 4-7)  contract the chunk on v_mfma_f32_32x32x16_bf16:
 //       weight fragments (pre-packed at plan time, one contiguous 1 KiB load
 //       each) straight from global memory, token fragments from LDS; the
 //       accumulators hold U^T = W Z^T (rows = output features, columns =
-//       tokens).  The epilogue adds the bias, applies the target RoPE to K,
-//       rounds to bf16 and stores 16-byte pieces of target rows directly.
+//       tokens).  After a tile's last chunk they add the bias, apply the
+//       target RoPE to K, round to bf16 and store 8-byte pieces of target
+//       rows directly from registers.
 //
 // K-chunks: the source features of a target layer are organised as RoPE
 // pairs (d, d + Ds/2) of every (mixed layer j, head h); chunk c holds the
@@ -55,31 +57,62 @@ struct FusedArgs {
   Strides ss;
   bf16_t* tgt[2];
   Strides ts;
-  const bf16x8* wp[2];      // packed fragments [Lt][dout/32][din/16][64 lanes]
+  const bf16x8* wp[2];      // packed bf16 fragments [Lt][dout/32][din/16][64 lanes]
+  const bf16x8* wh[2];      // the same as fp16 bit patterns (precision mode F16)
   const float* bias[2];     // [Lt][dout]
   const int32_t* layer_map; // [Lt][mix]
-  int32_t mix, hs, ds, ht, dt, din, dout;
+  int32_t mix, hs, ds, ht, dt, din, dout, lt;
   const double* fs;         // [ds/2] source theta_i / 2pi
   const double* ft;         // [dt/2] target theta_i / 2pi
   const int32_t* row_ptr;
   const int32_t* col_idx;
   const float* weight;
-  int32_t split_k;          // split the (de-rotated) K operand
-  int32_t split_v;          // split the (pooled) V operand
   int32_t n_tiles;          // N tiles per (layer, K|V)
   int32_t row_tiles;        // row tiles of this launch (all contexts)
+  int32_t total_tiles;      // row_tiles * n_tiles * 2 * Lt
   BatchArgs ba;
 };
 
 constexpr int fused_lds_bytes() { return 2 * 2 * kPlane * 2; }
+constexpr int kMaxLayerMap = 1024;  // target layers * mix held in LDS
+constexpr int kMaxHalfDim = 256;    // source head_dim / 2 held in LDS
 
-// Linear block id -> logical tile, so each XCD (blocks are dealt round-robin
-// to the 8 XCDs) sweeps one contiguous range of logical tiles and the weights
-// of a (layer, K|V) stay in that XCD's L2.
+// Workgroup id -> position in XCD-major order: workgroups are dealt
+// round-robin to the 8 XCDs, so this makes each XCD own one contiguous range.
 __device__ __forceinline__ int xcd_remap(int id, int total) {
   const int q = total / 8, r = total % 8;
   const int x = id % 8, slot = id / 8;
   return x * q + min(x, r) + slot;
+}
+
+struct Tile {
+  int l, kv, nt, b, t0, tt, rb;
+};
+
+// Tile order: layer slowest, then row tile, then N tile, K|V fastest (so a
+// contiguous range mixes K and V tiles and balances their different costs).
+__device__ __forceinline__ Tile decode_tile(const FusedArgs& a, int tau) {
+  Tile T;
+  T.kv = tau % 2;
+  int rest = tau / 2;
+  T.nt = rest % a.n_tiles;
+  rest /= a.n_tiles;
+  const int rt = rest % a.row_tiles;
+  T.l = rest / a.row_tiles;
+  T.b = find_context(a.ba, rt);
+  T.t0 = (rt - a.ba.tile_start[T.b]) * kMT;
+  T.tt = a.ba.t_tgt[T.b];
+  T.rb = a.ba.row_base[T.b];
+  return T;
+}
+
+// Workgroup barrier that orders LDS only: waits for this wave's LDS (and
+// scalar-load) counters, not for its outstanding global loads, so prefetched
+// data can stay in flight across steps.  The memory clobber keeps the
+// compiler from moving memory accesses across it.  (__syncthreads() would
+// also wait for every outstanding global load and store.)
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 __device__ __forceinline__ void unpack8(const uint4 v, float* x) {
@@ -91,17 +124,35 @@ __device__ __forceinline__ void unpack8(const uint4 v, float* x) {
   }
 }
 
-// Round 8 floats to bf16 (hardware RNE) and pack; optionally the residuals.
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+
+// Round 8 floats to bf16 (hardware round-to-nearest-even) and pack.
 __device__ __forceinline__ uint4 pack8(const float* z) {
   uint32_t o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
     bf16x2 p = {static_cast<__bf16>(z[2 * i]), static_cast<__bf16>(z[2 * i + 1])};
     o[i] = __builtin_bit_cast(uint32_t, p);
   }
   return make_uint4(o[0], o[1], o[2], o[3]);
 }
+
+typedef __attribute__((__vector_size__(2 * sizeof(_Float16)))) _Float16 f16x2;
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
+
+// Round 8 floats to fp16 (hardware round-to-nearest-even) and pack.
+__device__ __forceinline__ uint4 pack8_f16(const float* z) {
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f16x2 p = {static_cast<_Float16>(z[2 * i]), static_cast<_Float16>(z[2 * i + 1])};
+    o[i] = __builtin_bit_cast(uint32_t, p);
+  }
+  return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// Operand precision of computed operands (de-rotated K, pooled V).
+enum Prec { kBF16X2 = 0, kBF16 = 1, kF16 = 2 };
 
 __device__ __forceinline__ void residual8(const float* z, const uint4 hi, float* r) {
   float h[8];
@@ -110,101 +161,196 @@ __device__ __forceinline__ void residual8(const float* z, const uint4 hi, float*
   for (int i = 0; i < 8; ++i) r[i] = z[i] - h[i];
 }
 
-// Address of the first member of 8-pair group `grp` (pairs 8*grp .. 8*grp+7
-// of the flattened (j, h, d) list) for source token k, and its first freq.
+// First members of the 8-pair group `grp` (pairs 8*grp .. 8*grp+7 of the
+// flattened (j, h, d) list) at token 0; second members at p + ds/2.
 struct PairGroup {
-  const bf16_t* p;  // first members; second members at p + ds/2
-  int i0;           // frequency index of the first pair
+  const bf16_t* p;
+  int i0;  // frequency index of the first pair
 };
 
-__device__ __forceinline__ PairGroup pair_group(const FusedArgs& a, const bf16_t* src, int l,
-                                                int b, int grp) {
+__device__ __forceinline__ PairGroup pair_group(const FusedArgs& a, const int32_t* lmap,
+                                                const bf16_t* src, int l, int b, int grp) {
   const int half = a.ds / 2;
   const int pair = grp * 8;
   const int head_pairs = pair / half;  // (j, h) flattened
   const int i0 = pair % half;
   const int j = head_pairs / a.hs;
   const int h = head_pairs % a.hs;
-  const int ls = a.layer_map[l * a.mix + j];
+  const int ls = lmap[l * a.mix + j];
   PairGroup g;
   g.p = src + ls * a.ss.l + b * a.ss.b + h * a.ss.h + i0;
   g.i0 = i0;
   return g;
 }
 
-template <bool IDENT>
+// Alignment entries of the units of one producer thread within one tile.
+struct RowInfo {
+  int e0[kUnits], e1[kUnits], k0[kUnits];
+  float w0[kUnits];
+};
+
+// Whole 16-byte pieces of target rows from the staging buffer [token][kNT+8]
+// of tile Tc (staged column w*64 + p*32 + j holds feature c_p + j of pair
+// block 4*nt + w); thread `it` of 256.
+__device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, const bf16_t* st,
+                                           int it) {
+  constexpr int LDO = kNT + 8;
+  const int npb = a.dout / 64;
+  const int per_head = a.dt / 64;
+  bf16_t* dst = a.tgt[Tc.kv] + Tc.l * a.ts.l + Tc.b * a.ts.b;
+#pragma unroll 4
+  for (int i = 0; i < kMT * kNT / 8 / 256; ++i) {
+    const int pc = it + 256 * i;
+    const int r = pc / (kNT / 8);
+    const int sc8 = pc % (kNT / 8);   // staged column / 8
+    const int w = sc8 / 8;            // owning consumer wave (pair block)
+    const int pbw = Tc.nt * 4 + w;
+    const int t = Tc.t0 + r;
+    if (t < Tc.tt && pbw < npb) {
+      const int half = (sc8 / 4) % 2;
+      const int hpw = pbw / per_head;
+      const int colg = hpw * a.dt + 32 * (pbw % per_head) + half * (a.dt / 2) + (sc8 % 4) * 8;
+      const int hd = colg / a.dt;
+      const int d = colg % a.dt;
+      *reinterpret_cast<uint4*>(dst + hd * a.ts.h + t * a.ts.t + d) =
+          *reinterpret_cast<const uint4*>(st + r * LDO + sc8 * 8);
+    }
+  }
+}
+
+// IDENT: identity alignment.  CS_CACHE: the RoPE angles of a unit do not
+// change across the chunks of a tile (identity alignment and Ds = 128, where
+// every chunk is one head at the same frequencies), so they are computed once
+// per tile.
+//
+// Step schedule.  Each tile takes nch chunk steps followed by one epilogue
+// step; every step ends with a workgroup barrier and step s owns LDS buffer
+// s % 2.  In a chunk step the consumers contract the buffer the producers
+// filled during the previous step.  In the epilogue step the consumers stage
+// the finished tile in their buffer (a mid-step barrier separates staging
+// from the row stores), while the producers fill the other buffer with the
+// next tile's first chunk.  Producers prefetch raw source data two chunks
+// ahead into registers.
+//
+// PREC: how computed operands (de-rotated K, pooled V) reach the matrix
+// cores -- split into two bf16 terms (kBF16X2), rounded once to bf16 (kBF16)
+// or rounded once to fp16 and contracted against fp16 weights (kF16).  With
+// identity alignment V is already bf16 and goes through unchanged, except in
+// kF16 where every operand is fp16 (bf16 -> fp16 is exact in fp16's normal
+// range) so the consumers run a single contraction type.
+template <bool IDENT, bool CS_CACHE, int PREC>
 __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[fused_lds_bytes() / 2];
+  // layer map and source RoPE frequencies: per-lane lookups go to LDS, so no
+  // vector load inside the step loop can queue behind outstanding stores
+  __shared__ int32_t lmap[kMaxLayerMap];
+  __shared__ double fsl[kMaxHalfDim];
 
-  // ---- tile decode (XCD-aware) ----
-  const int logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int rt = logical % a.row_tiles;
-  int rest = logical / a.row_tiles;
-  const int nt = rest % a.n_tiles;
-  rest /= a.n_tiles;
-  const int kv = rest % 2;
-  const int l = rest / 2;
-  const int b = find_context(a.ba, rt);
-  const int t0 = (rt - a.ba.tile_start[b]) * kMT;
-  const int tt = a.ba.t_tgt[b];
-  const int row_base = a.ba.row_base[b];
-  const bool is_k = (kv == 0);
-  const bool split = is_k ? a.split_k : a.split_v;
-  const int nchunks = a.din / 128;
+  const int G = gridDim.x;
+  const int wid = xcd_remap(blockIdx.x, G);
+  const int tbeg = static_cast<int>(static_cast<int64_t>(wid) * a.total_tiles / G);
+  const int tend = static_cast<int>(static_cast<int64_t>(wid + 1) * a.total_tiles / G);
+  const int nch = a.din / 128;
+  const int spt = nch + 1;                    // steps per tile
+  const int nchunks = (tend - tbeg) * nch;    // chunk steps of this workgroup
+  const int nsteps = (tend - tbeg) * spt;
+  if (nsteps == 0) return;
   const int tid = threadIdx.x;
+  for (int i = tid; i < a.lt * a.mix; i += kThreads) lmap[i] = a.layer_map[i];
+  for (int i = tid; i < a.ds / 2; i += kThreads) fsl[i] = a.fs[i];
+  __syncthreads();
 
   if (tid < kProducers) {
     // =========================== producers ===========================
-    const int g = tid % 8;  // 8-pair group within the chunk
-    const bf16_t* src = a.src[kv];
-    int t_of[kUnits], e0_of[kUnits], e1_of[kUnits], k0_of[kUnits];
-    float w0_of[kUnits];
-#pragma unroll
-    for (int u = 0; u < kUnits; ++u) {
-      const int r = tid / 8 + 32 * u;
-      const int t = t0 + r;
-      t_of[u] = t;
-      if (IDENT) {
-        e0_of[u] = 0;
-        e1_of[u] = t < tt ? 1 : 0;
-        k0_of[u] = t;
-        w0_of[u] = 1.f;
-      } else {
-        int e0 = 0, e1 = 0;
-        if (t < tt) {
-          e0 = a.row_ptr[row_base + t];
-          e1 = a.row_ptr[row_base + t + 1];
-        }
-        e0_of[u] = e0;
-        e1_of[u] = e1;
-        k0_of[u] = e1 > e0 ? a.col_idx[e0] : 0;
-        w0_of[u] = e1 > e0 ? a.weight[e0] : 0.f;
-      }
-    }
+    const int g = tid % 8;  // 8-pair group within a chunk
 
-    // raw first-entry data of one chunk, prefetched a chunk ahead
-    uint4 raw0[kUnits], raw1[kUnits];
-    auto fetch = [&](int c) {
-      const PairGroup pg = pair_group(a, src, l, b, c * 8 + g);
+    auto row_info = [&](const Tile& T, RowInfo& ri) {
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
-        if (e1_of[u] > e0_of[u]) {
-          const bf16_t* p = pg.p + k0_of[u] * a.ss.t;
-          raw0[u] = *reinterpret_cast<const uint4*>(p);
-          raw1[u] = *reinterpret_cast<const uint4*>(p + a.ds / 2);
+        const int t = T.t0 + tid / 8 + 32 * u;
+        if (IDENT) {
+          ri.e0[u] = 0;
+          ri.e1[u] = t < T.tt ? 1 : 0;
+          ri.k0[u] = t;
+          ri.w0[u] = 1.f;
         } else {
-          raw0[u] = make_uint4(0, 0, 0, 0);
-          raw1[u] = make_uint4(0, 0, 0, 0);
+          int e0 = 0, e1 = 0;
+          if (t < T.tt) {
+            e0 = a.row_ptr[T.rb + t];
+            e1 = a.row_ptr[T.rb + t + 1];
+          }
+          ri.e0[u] = e0;
+          ri.e1[u] = e1;
+          ri.k0[u] = e1 > e0 ? a.col_idx[e0] : 0;
+          ri.w0[u] = e1 > e0 ? a.weight[e0] : 0.f;
         }
       }
     };
 
-    auto transform = [&](int c, bf16_t* hi, bf16_t* lo) {
-      const PairGroup pg = pair_group(a, src, l, b, c * 8 + g);
-      double f[8];
-      if (is_k) {
+    // Raw first-entry data of a chunk (global chunk index cs) and the row
+    // info it was fetched with; two such sets rotate (cs even / odd).
+    struct Raw {
+      uint4 x0[kUnits], x1[kUnits];
+      RowInfo ri;
+    };
+    Raw rA, rB;
+    int f_tile = -1;
+    Tile ftile{};
+    RowInfo fri;
+    auto fetch = [&](int cs, Raw& R) {
+      const int tau = tbeg + cs / nch;
+      const int c = cs % nch;
+      if (tau != f_tile) {
+        f_tile = tau;
+        ftile = decode_tile(a, tau);
+        if (!IDENT) row_info(ftile, fri);
+      }
+      if (!IDENT) R.ri = fri;
+      const PairGroup pg = pair_group(a, lmap, a.src[ftile.kv], ftile.l, ftile.b, c * 8 + g);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) f[i] = a.fs[pg.i0 + i];
+      for (int u = 0; u < kUnits; ++u) {
+        const int t = ftile.t0 + tid / 8 + 32 * u;  // identity: source token = t
+        const bool any = IDENT ? t < ftile.tt : fri.e1[u] > fri.e0[u];
+        if (any) {
+          const bf16_t* p = pg.p + (IDENT ? t : fri.k0[u]) * a.ss.t;
+          R.x0[u] = *reinterpret_cast<const uint4*>(p);
+          R.x1[u] = *reinterpret_cast<const uint4*>(p + a.ds / 2);
+        } else {
+          R.x0[u] = make_uint4(0, 0, 0, 0);
+          R.x1[u] = make_uint4(0, 0, 0, 0);
+        }
+      }
+    };
+
+    float csc[CS_CACHE ? kUnits : 1][8], css[CS_CACHE ? kUnits : 1][8];
+
+    auto transform = [&](int cs, const Raw& R, bf16_t* hi, bf16_t* lo) {
+      const int tau = tbeg + cs / nch;
+      const int c = cs % nch;
+      const Tile T = decode_tile(a, tau);
+      const bool is_k = T.kv == 0;
+      if (IDENT && !is_k && PREC != kF16) {
+        // identity-aligned V: the bf16 source rows are the operand
+#pragma unroll
+        for (int u = 0; u < kUnits; ++u) {
+          const int r = tid / 8 + 32 * u;
+          *reinterpret_cast<uint4*>(hi + r * kLDA + 8 * g) = R.x0[u];
+          *reinterpret_cast<uint4*>(hi + r * kLDA + 64 + 8 * g) = R.x1[u];
+        }
+        return;
+      }
+      const PairGroup pg = pair_group(a, lmap, a.src[T.kv], T.l, T.b, c * 8 + g);
+      double f[8];
+      if (is_k && (!CS_CACHE || c == 0)) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) f[i] = fsl[pg.i0 + i];
+      }
+      if (CS_CACHE && is_k && c == 0) {
+#pragma unroll
+        for (int u = 0; u < kUnits; ++u)
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            rope_cs(f[i], T.t0 + tid / 8 + 32 * u, csc[u][i], css[u][i]);
       }
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
@@ -212,25 +358,30 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         float z0[8], z1[8];
         {
           float x0[8], x1[8];
-          unpack8(raw0[u], x0);
-          unpack8(raw1[u], x1);
-          const int k = k0_of[u];
-          const float w = w0_of[u];
+          unpack8(R.x0[u], x0);
+          unpack8(R.x1[u], x1);
+          const int k = IDENT ? T.t0 + r : R.ri.k0[u];
+          const float w = IDENT ? 1.f : R.ri.w0[u];
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
             float y0 = x0[i], y1 = x1[i];
             if (is_k) {
-              float cs, sn;
-              rope_cs(f[i], k, cs, sn);
-              y0 = x0[i] * cs + x1[i] * sn;
-              y1 = x1[i] * cs - x0[i] * sn;
+              float cs_, sn;
+              if (CS_CACHE) {
+                cs_ = csc[u][i];
+                sn = css[u][i];
+              } else {
+                rope_cs(f[i], k, cs_, sn);
+              }
+              y0 = x0[i] * cs_ + x1[i] * sn;
+              y1 = x1[i] * cs_ - x0[i] * sn;
             }
             z0[i] = w * y0;
             z1[i] = w * y1;
           }
         }
         if (!IDENT) {
-          for (int e = e0_of[u] + 1; e < e1_of[u]; ++e) {
+          for (int e = R.ri.e0[u] + 1; e < R.ri.e1[u]; ++e) {
             const int k = a.col_idx[e];
             const float w = a.weight[e];
             const bf16_t* p = pg.p + k * a.ss.t;
@@ -241,20 +392,25 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
             for (int i = 0; i < 8; ++i) {
               float y0 = x0[i], y1 = x1[i];
               if (is_k) {
-                float cs, sn;
-                rope_cs(f[i], k, cs, sn);
-                y0 = x0[i] * cs + x1[i] * sn;
-                y1 = x1[i] * cs - x0[i] * sn;
+                float cs_, sn;
+                rope_cs(f[i], k, cs_, sn);
+                y0 = x0[i] * cs_ + x1[i] * sn;
+                y1 = x1[i] * cs_ - x0[i] * sn;
               }
               z0[i] += w * y0;
               z1[i] += w * y1;
             }
           }
         }
+        if (PREC == kF16) {
+          *reinterpret_cast<uint4*>(hi + r * kLDA + 8 * g) = pack8_f16(z0);
+          *reinterpret_cast<uint4*>(hi + r * kLDA + 64 + 8 * g) = pack8_f16(z1);
+          continue;
+        }
         const uint4 h0 = pack8(z0), h1 = pack8(z1);
         *reinterpret_cast<uint4*>(hi + r * kLDA + 8 * g) = h0;
         *reinterpret_cast<uint4*>(hi + r * kLDA + 64 + 8 * g) = h1;
-        if (split) {
+        if (PREC == kBF16X2) {
           float d0[8], d1[8];
           residual8(z0, h0, d0);
           residual8(z1, h1, d1);
@@ -264,125 +420,231 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       }
     };
 
-    fetch(0);
-    transform(0, lds, lds + kPlane);
-    if (nchunks > 1) fetch(1);
-    __syncthreads();
-    for (int c = 0; c < nchunks; ++c) {
-      if (c + 1 < nchunks) {
-        bf16_t* buf = lds + ((c + 1) % 2) * 2 * kPlane;
-        transform(c + 1, buf, buf + kPlane);
-        if (c + 2 < nchunks) fetch(c + 2);
+    // chunk cs is consumed at step s(cs) = (cs / nch) * spt + cs % nch and
+    // written into buffer s(cs) % 2 during the step before.
+    auto step_of = [&](int cs) { return (cs / nch) * spt + cs % nch; };
+    fetch(0, rA);
+    if (nchunks > 1) fetch(1, rB);
+    transform(0, rA, lds, lds + kPlane);
+    if (nchunks > 2) fetch(2, rA);
+    lds_barrier();
+    int next = 1;  // next chunk to transform
+    for (int s = 0; s < nsteps; ++s) {
+      if (next < nchunks && step_of(next) == s + 1) {
+        bf16_t* buf = lds + ((s + 1) % 2) * 2 * kPlane;
+        if (next & 1) {
+          transform(next, rB, buf, buf + kPlane);
+          if (next + 2 < nchunks) fetch(next + 2, rB);
+        } else {
+          transform(next, rA, buf, buf + kPlane);
+          if (next + 2 < nchunks) fetch(next + 2, rA);
+        }
+        ++next;
       }
-      __syncthreads();
+      if (s % spt == nch) {
+        // epilogue step: the consumers staged the finished tile in buffer
+        // s % 2; write its rows (the consumers issue no global stores, so
+        // their weight loads never wait behind store completion)
+        lds_barrier();
+        store_rows(a, decode_tile(a, tbeg + s / spt), lds + (s % 2) * 2 * kPlane, tid);
+      }
+      lds_barrier();
     }
     return;
   }
 
   // =========================== consumers ===========================
   const int lane = tid & 63;
-  const int cw = (tid - kProducers) >> 6;  // consumer wave 0..3
+  const int ct = tid - kProducers;        // consumer thread 0..255
+  const int cw = ct >> 6;                 // consumer wave 0..3
   const int npb = a.dout / 64;
-  const int pb = nt * 4 + cw;
-  const bool wave_on = pb < npb;
   const int per_head = a.dt / 64;
-  const int hp = wave_on ? pb / per_head : 0;
-  const int q = wave_on ? pb % per_head : 0;
-  const int c0 = hp * a.dt + 32 * q;   // first feature of the low half
-  const int c1 = c0 + a.dt / 2;        // its RoPE partners
   const int KSALL = a.din / 16;
-  const bf16x8* w0p =
-      a.wp[kv] + (static_cast<int64_t>(l) * (a.dout / 32) + c0 / 32) * KSALL * 64 + lane;
-  const bf16x8* w1p =
-      a.wp[kv] + (static_cast<int64_t>(l) * (a.dout / 32) + c1 / 32) * KSALL * 64 + lane;
+  const int trow = lane % 32;
+  const int tcol = 8 * (lane / 32);
+  const int fq = 4 * (lane / 32);
+  constexpr int LDO = kNT + 8;            // staging row stride (bf16)
+
+  struct Blocks {
+    bool on;
+    int c0, c1, q, hp;
+    const bf16x8* w0p;
+    const bf16x8* w1p;
+  };
+  auto blocks = [&](const Tile& T, int w) {
+    Blocks B;
+    const int pb = T.nt * 4 + w;
+    B.on = pb < npb;
+    B.hp = B.on ? pb / per_head : 0;
+    B.q = B.on ? pb % per_head : 0;
+    B.c0 = B.hp * a.dt + 32 * B.q;
+    B.c1 = B.c0 + a.dt / 2;
+    const bf16x8* wsel = PREC == kF16 ? a.wh[T.kv] : a.wp[T.kv];
+    const bf16x8* base = wsel + static_cast<int64_t>(T.l) * (a.dout / 32) * KSALL * 64;
+    B.w0p = base + static_cast<int64_t>(B.c0 / 32) * KSALL * 64 + lane;
+    B.w1p = base + static_cast<int64_t>(B.c1 / 32) * KSALL * 64 + lane;
+    return B;
+  };
 
   f32x16 acc[4][2];
-#pragma unroll
-  for (int m = 0; m < 4; ++m)
-#pragma unroll
-    for (int p = 0; p < 2; ++p)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[m][p][v] = 0.f;
-
   bf16x8 wf[8][2];
-  auto load_w = [&](int c) {
-    if (!wave_on) return;
+  auto load_w = [&](const Blocks& B, int c) {
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
-      wf[ks][0] = w0p[(c * 8 + ks) * 64];
-      wf[ks][1] = w1p[(c * 8 + ks) * 64];
+      wf[ks][0] = B.w0p[(c * 8 + ks) * 64];
+      wf[ks][1] = B.w1p[(c * 8 + ks) * 64];
     }
   };
 
-  load_w(0);
-  __syncthreads();
-  const int trow = lane % 32;
-  const int tcol = 8 * (lane / 32);
-  for (int c = 0; c < nchunks; ++c) {
-    const bf16_t* hi = lds + (c % 2) * 2 * kPlane;
-    const bf16_t* lo = hi + kPlane;
-    if (wave_on) {
+  // Bias, target RoPE on K, bf16, into the staging buffer [token][256 + 8]:
+  // lane holds, for token column lane%32 of token block m, the features
+  // 8*(v/4) + 4*(lane/32) + v%4 (v < 16) of blocks c0 and c1; staged at
+  // column cw*64 + p*32 + feature offset.  Bias and frequencies come from
+  // wave-uniform scalar loads (read-only data).
+  auto stage = [&](const Tile& Tc, const Blocks& B, bf16_t* st) {
+    typedef const __attribute__((address_space(4))) float* cfloat_p;
+    typedef const __attribute__((address_space(4))) double* cdouble_p;
+    const int l_u = __builtin_amdgcn_readfirstlane(Tc.l);
+    const int kv_u = __builtin_amdgcn_readfirstlane(Tc.kv);
+    const int c0u = __builtin_amdgcn_readfirstlane(B.c0);
+    const int c1u = __builtin_amdgcn_readfirstlane(B.c1);
+    const int qu = __builtin_amdgcn_readfirstlane(B.q);
+    const cfloat_p bl = (cfloat_p)(a.bias[kv_u] + static_cast<int64_t>(l_u) * a.dout);
+    const cdouble_p fr = (cdouble_p)(a.ft);
+    const bool upper = lane >= 32;
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
+    for (int g4 = 0; g4 < 4; ++g4) {
+      float b0[8], b1[8];
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          const int off = (m * 32 + trow) * kLDA + ks * 16 + tcol;
-          const bf16x8 zh = *reinterpret_cast<const bf16x8*>(hi + off);
-          acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][0], zh, acc[m][0], 0, 0, 0);
-          acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][1], zh, acc[m][1], 0, 0, 0);
-          if (split) {
-            const bf16x8 zl = *reinterpret_cast<const bf16x8*>(lo + off);
-            acc[m][0] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][0], zl, acc[m][0], 0, 0, 0);
-            acc[m][1] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][1], zl, acc[m][1], 0, 0, 0);
+      for (int k = 0; k < 8; ++k) {
+        b0[k] = bl[c0u + 8 * g4 + k];
+        b1[k] = bl[c1u + 8 * g4 + k];
+      }
+      double f8[8];
+      if (kv_u == 0) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) f8[k] = fr[32 * qu + 8 * g4 + k];
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int row = m * 32 + lane % 32;
+        float u0[4], u1[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          u0[i] = acc[m][0][4 * g4 + i] + (upper ? b0[4 + i] : b0[i]);
+          u1[i] = acc[m][1][4 * g4 + i] + (upper ? b1[4 + i] : b1[i]);
+        }
+        if (kv_u == 0) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float cs, sn;
+            rope_cs(upper ? f8[4 + i] : f8[i], Tc.t0 + row, cs, sn);
+            const float y0 = u0[i] * cs - u1[i] * sn;
+            const float y1 = u1[i] * cs + u0[i] * sn;
+            u0[i] = y0;
+            u1[i] = y1;
+          }
+        }
+        const bf16x2 p00 = {static_cast<__bf16>(u0[0]), static_cast<__bf16>(u0[1])};
+        const bf16x2 p01 = {static_cast<__bf16>(u0[2]), static_cast<__bf16>(u0[3])};
+        const bf16x2 p10 = {static_cast<__bf16>(u1[0]), static_cast<__bf16>(u1[1])};
+        const bf16x2 p11 = {static_cast<__bf16>(u1[2]), static_cast<__bf16>(u1[3])};
+        bf16_t* sp = st + row * LDO + cw * 64 + 8 * g4 + fq;
+        *reinterpret_cast<uint2*>(sp) =
+            make_uint2(__builtin_bit_cast(uint32_t, p00), __builtin_bit_cast(uint32_t, p01));
+        *reinterpret_cast<uint2*>(sp + 32) =
+            make_uint2(__builtin_bit_cast(uint32_t, p10), __builtin_bit_cast(uint32_t, p11));
+      }
+    }
+  };
+
+  Tile T = decode_tile(a, tbeg);
+  Blocks B = blocks(T, cw);
+  if (B.on) load_w(B, 0);
+  lds_barrier();
+  int cs = 0;  // global chunk index
+  for (int s = 0; s < nsteps; ++s) {
+    bf16_t* buf = lds + (s % 2) * 2 * kPlane;
+    if (s % spt < nch) {
+      // ---------------- chunk step ----------------
+      const int c = s % spt;
+      if (c == 0) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+          for (int p = 0; p < 2; ++p)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[m][p][v] = 0.f;
+      }
+      const bool computed = T.kv == 0 || !IDENT;
+      if (B.on) {
+        const bf16_t* hi = buf;
+        const bf16_t* lo = buf + kPlane;
+        if (PREC == kF16) {
+#pragma unroll
+          for (int ks = 0; ks < 8; ++ks) {
+            f16x8 zh[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+              zh[m] = *reinterpret_cast<const f16x8*>(hi + (m * 32 + trow) * kLDA + ks * 16 + tcol);
+            const f16x8 w0 = __builtin_bit_cast(f16x8, wf[ks][0]);
+            const f16x8 w1 = __builtin_bit_cast(f16x8, wf[ks][1]);
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w0, zh[m], acc[m][0], 0, 0, 0);
+              acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w1, zh[m], acc[m][1], 0, 0, 0);
+            }
+          }
+        } else {
+          const bool split = PREC == kBF16X2 && computed;
+#pragma unroll
+          for (int ks = 0; ks < 8; ++ks) {
+            bf16x8 zh[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+              zh[m] =
+                  *reinterpret_cast<const bf16x8*>(hi + (m * 32 + trow) * kLDA + ks * 16 + tcol);
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              acc[m][0] =
+                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][0], zh[m], acc[m][0], 0, 0, 0);
+              acc[m][1] =
+                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][1], zh[m], acc[m][1], 0, 0, 0);
+            }
+            if (split) {
+#pragma unroll
+              for (int m = 0; m < 4; ++m)
+                zh[m] = *reinterpret_cast<const bf16x8*>(lo + (m * 32 + trow) * kLDA + ks * 16 +
+                                                         tcol);
+#pragma unroll
+              for (int m = 0; m < 4; ++m) {
+                acc[m][0] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][0], zh[m], acc[m][0], 0, 0, 0);
+                acc[m][1] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][1], zh[m], acc[m][1], 0, 0, 0);
+              }
+            }
           }
         }
       }
-      if (c + 1 < nchunks) load_w(c + 1);
-    }
-    __syncthreads();
-  }
-  if (!wave_on) return;
-
-  // ---- epilogue: bias, target RoPE on K, bf16, direct 8-byte stores ----
-  // lane holds, for token column lane%32 of token block m, the features
-  // f = 8*(v/4) + 4*(lane/32) + v%4 (v < 16) of blocks c0 and c1.
-  const float* bl = a.bias[kv] + static_cast<int64_t>(l) * a.dout;
-  bf16_t* dst = a.tgt[kv] + l * a.ts.l + b * a.ts.b;
-  const int fq = 4 * (lane / 32);
-#pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const int t = t0 + m * 32 + lane % 32;
-    if (t >= tt) continue;
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      float u0[4], u1[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int fo = 8 * g4 + fq + i;  // feature offset within the 32-block
-        u0[i] = acc[m][0][4 * g4 + i] + bl[c0 + fo];
-        u1[i] = acc[m][1][4 * g4 + i] + bl[c1 + fo];
-        if (is_k) {
-          float cs, sn;
-          rope_cs(a.ft[32 * q + fo], t, cs, sn);
-          const float y0 = u0[i] * cs - u1[i] * sn;
-          const float y1 = u1[i] * cs + u0[i] * sn;
-          u0[i] = y0;
-          u1[i] = y1;
-        }
+      ++cs;
+      // weights of the next chunk (possibly of the next tile)
+      if (cs < nchunks) {
+        const int cn = cs % nch;
+        Blocks Bn = B;
+        if (cn == 0) Bn = blocks(decode_tile(a, tbeg + cs / nch), cw);
+        if (Bn.on) load_w(Bn, cn);
       }
-      typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
-      const bf16x2 p00 = {static_cast<__bf16>(u0[0]), static_cast<__bf16>(u0[1])};
-      const bf16x2 p01 = {static_cast<__bf16>(u0[2]), static_cast<__bf16>(u0[3])};
-      const bf16x2 p10 = {static_cast<__bf16>(u1[0]), static_cast<__bf16>(u1[1])};
-      const bf16x2 p11 = {static_cast<__bf16>(u1[2]), static_cast<__bf16>(u1[3])};
-      const int d0 = 32 * q + 8 * g4 + fq;  // dim within target head hp
-      bf16_t* rowp = dst + hp * a.ts.h + t * a.ts.t;
-      *reinterpret_cast<uint2*>(rowp + d0) =
-          make_uint2(__builtin_bit_cast(uint32_t, p00), __builtin_bit_cast(uint32_t, p01));
-      *reinterpret_cast<uint2*>(rowp + a.dt / 2 + d0) =
-          make_uint2(__builtin_bit_cast(uint32_t, p10), __builtin_bit_cast(uint32_t, p11));
+      lds_barrier();
+    } else {
+      // ---------------- epilogue step ----------------
+      if (B.on) stage(T, B, buf);
+      lds_barrier();  // staging complete; the producers store the rows
+      lds_barrier();
+      if (cs < nchunks) {
+        T = decode_tile(a, tbeg + cs / nch);
+        B = blocks(T, cw);
+      }
     }
   }
 }

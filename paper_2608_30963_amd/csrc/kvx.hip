@@ -43,12 +43,14 @@ struct kvx_plan {
   int32_t precision = KVX_PREC_BF16X2;
   int32_t din = 0, dout = 0;
   int kernel = kTiled;
+  int n_cu = 0;                  // compute units of the plan's device
   int64_t bytes = 0;
   // device memory owned by the plan
   int32_t* layer_map = nullptr;  // [Lt*mix]
   double* fs = nullptr;          // [Ds/2] theta_i / 2pi (zeros when RoPE is off)
   double* ft = nullptr;          // [Dt/2]
   void* w[2] = {nullptr, nullptr};  // tiled: [Lt][dout][din]; fused: packed fragments
+  void* wh[2] = {nullptr, nullptr}; // fused, precision F16: packed fp16 fragments
   float* bias[2] = {nullptr, nullptr};
   void* block = nullptr;         // single allocation backing all of the above
 };
@@ -76,7 +78,9 @@ std::vector<double> rope_table(const kvx_model& m) {
 
 bool fused_supported(const kvx_plan& p) {
   return p.dtype == KVX_BF16 && p.src.head_dim % 16 == 0 && p.din % 128 == 0 &&
-         p.tgt.head_dim % 64 == 0 && p.dout % 64 == 0;
+         p.tgt.head_dim % 64 == 0 && p.dout % 64 == 0 &&
+         p.src.head_dim / 2 <= kMaxHalfDim &&
+         int64_t(p.tgt.n_layers) * p.mix <= kMaxLayerMap;
 }
 
 // Input feature held in K-slot `k` of the fused kernel: chunk c = k / 128 holds
@@ -117,7 +121,9 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   if (!d || !out || !d->layer_map || !d->w_k || !d->w_v) return KVX_EINVAL;
   if (!valid_model(d->src) || !valid_model(d->tgt) || d->mix < 1) return KVX_EINVAL;
   if (d->dtype != KVX_F32 && d->dtype != KVX_BF16) return KVX_EINVAL;
-  if (d->precision != KVX_PREC_BF16X2 && d->precision != KVX_PREC_BF16) return KVX_EINVAL;
+  if (d->precision != KVX_PREC_BF16X2 && d->precision != KVX_PREC_BF16 &&
+      d->precision != KVX_PREC_F16)
+    return KVX_EINVAL;
   if (d->src.head_dim % 2 || d->tgt.head_dim % 2) return KVX_EUNSUPPORTED;
   const int64_t lt = d->tgt.n_layers;
   for (int64_t i = 0; i < lt * d->mix; ++i)
@@ -151,6 +157,8 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
 
   hipError_t e = hipGetDevice(&p->device);
   if (e != hipSuccess) return fail(hip_fail(e));
+  e = hipDeviceGetAttribute(&p->n_cu, hipDeviceAttributeMultiprocessorCount, p->device);
+  if (e != hipSuccess) return fail(hip_fail(e));
 
   const size_t esz = d->dtype == KVX_F32 ? 4 : 2;
   const size_t wbytes = size_t(lt) * dout64 * din64 * esz;
@@ -158,7 +166,11 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   const size_t mbytes = size_t(lt) * d->mix * sizeof(int32_t);
   const size_t fsb = d->src.head_dim / 2 * sizeof(double);
   const size_t ftb = d->tgt.head_dim / 2 * sizeof(double);
-  size_t off_w0 = 0, off_w1 = align256(wbytes), off_b0 = off_w1 + align256(wbytes);
+  const bool want_f16 = p->kernel == kFused && d->precision == KVX_PREC_F16;
+  const size_t hbytes = want_f16 ? wbytes : 0;
+  size_t off_w0 = 0, off_w1 = align256(wbytes);
+  size_t off_h0 = off_w1 + align256(wbytes), off_h1 = off_h0 + align256(hbytes);
+  size_t off_b0 = off_h1 + align256(hbytes);
   size_t off_b1 = off_b0 + align256(bbytes), off_m = off_b1 + align256(bbytes);
   size_t off_fs = off_m + align256(mbytes), off_ft = off_fs + align256(fsb);
   size_t total = off_ft + align256(ftb);
@@ -168,6 +180,10 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   char* base = static_cast<char*>(p->block);
   p->w[0] = base + off_w0;
   p->w[1] = base + off_w1;
+  if (want_f16) {
+    p->wh[0] = base + off_h0;
+    p->wh[1] = base + off_h1;
+  }
   p->bias[0] = reinterpret_cast<float*>(base + off_b0);
   p->bias[1] = reinterpret_cast<float*>(base + off_b1);
   p->layer_map = reinterpret_cast<int32_t*>(base + off_m);
@@ -205,6 +221,22 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
     }
     e = hipMemcpy(p->w[kv], up, wbytes, hipMemcpyHostToDevice);
     if (e != hipSuccess) return fail(hip_fail(e));
+    if (want_f16) {
+      // the same fragments as fp16 (exact for bf16 values in the fp16 normal
+      // range; smaller magnitudes round to the nearest fp16 subnormal)
+      std::vector<uint16_t> h(wbytes / 2);
+      const uint16_t* src16 = static_cast<const uint16_t*>(up);
+      for (size_t i = 0; i < h.size(); ++i) {
+        uint32_t u = static_cast<uint32_t>(src16[i]) << 16;
+        float f;
+        std::memcpy(&f, &u, sizeof f);
+        if (!(std::fabs(f) <= 65504.0f)) return fail(KVX_EUNSUPPORTED);
+        _Float16 hv = static_cast<_Float16>(f);
+        std::memcpy(&h[i], &hv, sizeof hv);
+      }
+      e = hipMemcpy(p->wh[kv], h.data(), wbytes, hipMemcpyHostToDevice);
+      if (e != hipSuccess) return fail(hip_fail(e));
+    }
   }
   const float* bsrc[2] = {d->b_k, d->b_v};
   for (int kv = 0; kv < 2; ++kv) {
@@ -239,7 +271,7 @@ kvx_status kvx_plan_query(const kvx_plan* p, kvx_plan_info* info) {
   info->tile_rows = p->kernel == kFused ? kMT : 0;
   info->tile_cols = p->kernel == kFused ? kNT : 0;
   info->threads = p->kernel == kFused ? kThreads : 256;
-  info->split_k = p->kernel == kFused && p->precision == KVX_PREC_BF16X2;
+  info->precision = p->precision;
   info->weight_bytes = p->bytes;
   return KVX_OK;
 }
@@ -247,6 +279,25 @@ kvx_status kvx_plan_query(const kvx_plan* p, kvx_plan_info* info) {
 }  // extern "C"
 
 namespace {
+
+template <int PREC>
+void launch_fused_p(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
+  if (identity && ds128)
+    fused_kernel<true, true, PREC><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  else if (identity)
+    fused_kernel<true, false, PREC><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  else
+    fused_kernel<false, false, PREC><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+}
+
+void launch_fused(bool identity, bool ds128, int precision, int grid, hipStream_t st,
+                  const FusedArgs& a) {
+  switch (precision) {
+    case KVX_PREC_BF16: launch_fused_p<kBF16>(identity, ds128, grid, st, a); break;
+    case KVX_PREC_F16: launch_fused_p<kF16>(identity, ds128, grid, st, a); break;
+    default: launch_fused_p<kBF16X2>(identity, ds128, grid, st, a); break;
+  }
+}
 
 int tiled_rows(int din) {
   int r = 16384 / (din > 0 ? din : 1);
@@ -372,6 +423,8 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       a.ts = ts;
       a.wp[0] = static_cast<const bf16x8*>(p->w[0]);
       a.wp[1] = static_cast<const bf16x8*>(p->w[1]);
+      a.wh[0] = static_cast<const bf16x8*>(p->wh[0]);
+      a.wh[1] = static_cast<const bf16x8*>(p->wh[1]);
       a.bias[0] = p->bias[0];
       a.bias[1] = p->bias[1];
       a.layer_map = p->layer_map;
@@ -382,22 +435,22 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       a.din = p->din;
       a.dout = p->dout;
       a.ds = static_cast<int32_t>(Ds);
+      a.lt = static_cast<int32_t>(Lt);
       a.fs = p->fs;
       a.ft = p->ft;
       a.row_ptr = io.row_ptr;
       a.col_idx = io.col_idx;
       a.weight = io.weight;
-      a.split_k = p->precision == KVX_PREC_BF16X2;
-      a.split_v = p->precision == KVX_PREC_BF16X2 && !identity;
       a.n_tiles = (p->dout / 64 + 3) / 4;
       a.row_tiles = tiles;
       a.ba = ba;
-      const int64_t grid = int64_t(tiles) * a.n_tiles * 2 * Lt;
-      if (grid > INT32_MAX) return KVX_ESHAPE;
-      if (identity)
-        fused_kernel<true><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
-      else
-        fused_kernel<false><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+      const int64_t total = int64_t(tiles) * a.n_tiles * 2 * Lt;
+      if (total > INT32_MAX) return KVX_ESHAPE;
+      a.total_tiles = static_cast<int32_t>(total);
+      // persistent: one workgroup per compute unit (the kernel's LDS use
+      // allows exactly one), each walking a contiguous range of tiles
+      const int grid = static_cast<int>(total < p->n_cu ? total : p->n_cu);
+      launch_fused(identity, Ds == 128, p->precision, grid, st, a);
     } else {
       const size_t lds = size_t(rows_per_tile) * p->din * sizeof(float);
       if (p->dtype == KVX_F32) {

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(HERE, "libkvx.so")
 
 KVX_OK, KVX_EINVAL, KVX_ESHAPE, KVX_EUNSUPPORTED, KVX_ENOMEM, KVX_EHIP, KVX_EDATA = range(7)
 KVX_F32, KVX_BF16 = 0, 1
-KVX_PREC_BF16X2, KVX_PREC_BF16 = 0, 1
+KVX_PREC_BF16X2, KVX_PREC_BF16, KVX_PREC_F16 = 0, 1, 2
 
 # Exported C symbols, as declared in include/kvx.h.
 SYMBOLS = ("kvx_plan_create", "kvx_translate", "kvx_plan_destroy", "kvx_status_string",
@@ -56,7 +56,7 @@ class IO(C.Structure):
 
 class PlanInfo(C.Structure):
     _fields_ = [("kernel", C.c_int32), ("tile_rows", C.c_int32), ("tile_cols", C.c_int32),
-                ("threads", C.c_int32), ("split_k", C.c_int32), ("weight_bytes", C.c_int64)]
+                ("threads", C.c_int32), ("precision", C.c_int32), ("weight_bytes", C.c_int64)]
 
 
 _lib = None

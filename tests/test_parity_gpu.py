@@ -53,6 +53,11 @@ def test_config5_small():
     _full(S.config(5, src_tokens=384), expect_kernel=1)
 
 
+@pytest.mark.parametrize("cfg,T,B", [(2, 300, 1), (3, 700, 2), (4, 1024, 8), (5, 384, 1)])
+def test_f16_operand_mode(cfg, T, B):
+    _full(S.config(cfg, src_tokens=T, batch=B), precision=kvx.KVX_PREC_F16, expect_kernel=1)
+
+
 def test_config2_single_precision_mode_no_outliers():
     # single bf16 rounding of the operand is within tolerance without outliers
     _full(S.config(2, src_tokens=260).replace(outliers=0), precision=kvx.KVX_PREC_BF16)
@@ -104,6 +109,10 @@ def _sampled(spec, precision=kvx.KVX_PREC_BF16X2, n_layers_pick=3):
 
 def test_config2_full_size_sampled():
     _sampled(S.config(2))
+
+
+def test_config2_full_size_sampled_f16():
+    _sampled(S.config(2), precision=kvx.KVX_PREC_F16)
 
 
 def test_config3_full_size_sampled():
