@@ -297,7 +297,10 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     int f_tile = -1;
     Tile ftile{};
     RowInfo fri;
-    auto fetch = [&](int cs, Raw& R) {
+    // Address of chunk cs's first 8-pair group for this thread (and the tile's
+    // row info).  Done before the step's LDS writes: its LDS and scalar
+    // lookups then do not wait for those writes to drain.
+    auto fetch_addr = [&](int cs) -> const bf16_t* {
       const int tau = tbeg + cs / nch;
       const int c = cs % nch;
       if (tau != f_tile) {
@@ -305,8 +308,12 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         ftile = decode_tile(a, tau);
         if (!IDENT) row_info(ftile, fri);
       }
+      return pair_group(a, lmap, a.src[ftile.kv], ftile.l, ftile.b, c * 8 + g).p;
+    };
+    auto fetch_issue = [&](const bf16_t* gp, Raw& R) {
       if (!IDENT) R.ri = fri;
-      const PairGroup pg = pair_group(a, lmap, a.src[ftile.kv], ftile.l, ftile.b, c * 8 + g);
+      PairGroup pg;
+      pg.p = gp;
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
         const int t = ftile.t0 + tid / 8 + 32 * u;  // identity: source token = t
@@ -423,21 +430,26 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // chunk cs is consumed at step s(cs) = (cs / nch) * spt + cs % nch and
     // written into buffer s(cs) % 2 during the step before.
     auto step_of = [&](int cs) { return (cs / nch) * spt + cs % nch; };
-    fetch(0, rA);
-    if (nchunks > 1) fetch(1, rB);
-    transform(0, rA, lds, lds + kPlane);
-    if (nchunks > 2) fetch(2, rA);
+    fetch_issue(fetch_addr(0), rA);
+    if (nchunks > 1) fetch_issue(fetch_addr(1), rB);
+    {
+      const bf16_t* gp = nchunks > 2 ? fetch_addr(2) : nullptr;
+      transform(0, rA, lds, lds + kPlane);
+      if (nchunks > 2) fetch_issue(gp, rA);
+    }
     lds_barrier();
     int next = 1;  // next chunk to transform
     for (int s = 0; s < nsteps; ++s) {
       if (next < nchunks && step_of(next) == s + 1) {
         bf16_t* buf = lds + ((s + 1) % 2) * 2 * kPlane;
+        const bool more = next + 2 < nchunks;
+        const bf16_t* gp = more ? fetch_addr(next + 2) : nullptr;
         if (next & 1) {
           transform(next, rB, buf, buf + kPlane);
-          if (next + 2 < nchunks) fetch(next + 2, rB);
+          if (more) fetch_issue(gp, rB);
         } else {
           transform(next, rA, buf, buf + kPlane);
-          if (next + 2 < nchunks) fetch(next + 2, rA);
+          if (more) fetch_issue(gp, rA);
         }
         ++next;
       }
@@ -581,19 +593,28 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         const bf16_t* hi = buf;
         const bf16_t* lo = buf + kPlane;
         if (PREC == kF16) {
+          // token fragments of k-step ks+1 are read while the MFMAs of ks run
+          f16x8 zc[4], zn[4];
+#pragma unroll
+          for (int m = 0; m < 4; ++m)
+            zc[m] = *reinterpret_cast<const f16x8*>(hi + (m * 32 + trow) * kLDA + tcol);
 #pragma unroll
           for (int ks = 0; ks < 8; ++ks) {
-            f16x8 zh[4];
+            if (ks + 1 < 8) {
 #pragma unroll
-            for (int m = 0; m < 4; ++m)
-              zh[m] = *reinterpret_cast<const f16x8*>(hi + (m * 32 + trow) * kLDA + ks * 16 + tcol);
+              for (int m = 0; m < 4; ++m)
+                zn[m] = *reinterpret_cast<const f16x8*>(hi + (m * 32 + trow) * kLDA +
+                                                        (ks + 1) * 16 + tcol);
+            }
             const f16x8 w0 = __builtin_bit_cast(f16x8, wf[ks][0]);
             const f16x8 w1 = __builtin_bit_cast(f16x8, wf[ks][1]);
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
-              acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w0, zh[m], acc[m][0], 0, 0, 0);
-              acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w1, zh[m], acc[m][1], 0, 0, 0);
+              acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w0, zc[m], acc[m][0], 0, 0, 0);
+              acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w1, zc[m], acc[m][1], 0, 0, 0);
             }
+#pragma unroll
+            for (int m = 0; m < 4; ++m) zc[m] = zn[m];
           }
         } else {
           const bool split = PREC == kBF16X2 && computed;
