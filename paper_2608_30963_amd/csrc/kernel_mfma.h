@@ -70,8 +70,14 @@ struct FusedArgs {
   int32_t n_tiles;          // N tiles per (layer, K|V)
   int32_t row_tiles;        // row tiles of this launch (all contexts)
   int32_t total_tiles;      // row_tiles * n_tiles * 2 * Lt
+  const bf16_t* zsink;      // kSinkBytes of zeros: source of lanes without data
+  bf16_t* trash;            // kSinkBytes never read: target of lanes without a row
   BatchArgs ba;
 };
+
+// Size of each of the two sink areas: covers the second member of a pair
+// group (Ds/2 + 8 elements) for Ds <= 2*kMaxHalfDim, and one 16-byte store.
+constexpr int kSinkBytes = 2048;
 
 constexpr int fused_lds_bytes() { return 2 * 2 * kPlane * 2; }
 constexpr int kMaxLayerMap = 1024;  // target layers * mix held in LDS
@@ -206,15 +212,16 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
     const int w = sc8 / 8;            // owning consumer wave (pair block)
     const int pbw = Tc.nt * 4 + w;
     const int t = Tc.t0 + r;
-    if (t < Tc.tt && pbw < npb) {
-      const int half = (sc8 / 4) % 2;
-      const int hpw = pbw / per_head;
-      const int colg = hpw * a.dt + 32 * (pbw % per_head) + half * (a.dt / 2) + (sc8 % 4) * 8;
-      const int hd = colg / a.dt;
-      const int d = colg % a.dt;
-      *reinterpret_cast<uint4*>(dst + hd * a.ts.h + t * a.ts.t + d) =
-          *reinterpret_cast<const uint4*>(st + r * LDO + sc8 * 8);
-    }
+    // rows past the context's end and pair blocks past dout go to the trash
+    // area, so the store is unconditional
+    const int half = (sc8 / 4) % 2;
+    const int hpw = pbw / per_head;
+    const int colg = hpw * a.dt + 32 * (pbw % per_head) + half * (a.dt / 2) + (sc8 % 4) * 8;
+    const int hd = colg / a.dt;
+    const int d = colg % a.dt;
+    bf16_t* q = dst + hd * a.ts.h + t * a.ts.t + d;
+    q = (t < Tc.tt && pbw < npb) ? q : a.trash;
+    *reinterpret_cast<uint4*>(q) = *reinterpret_cast<const uint4*>(st + r * LDO + sc8 * 8);
   }
 }
 
@@ -274,15 +281,20 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
           ri.k0[u] = t;
           ri.w0[u] = 1.f;
         } else {
-          int e0 = 0, e1 = 0;
-          if (t < T.tt) {
-            e0 = a.row_ptr[T.rb + t];
-            e1 = a.row_ptr[T.rb + t + 1];
-          }
+          // unconditional loads: rows past the context's end read the last
+          // row's pointers (a tile holds at least one row) and are then
+          // emptied; empty rows read their first entry from the zero sink
+          const int tc = t < T.tt ? t : T.tt - 1;
+          const int e0 = a.row_ptr[T.rb + tc];
+          int e1 = a.row_ptr[T.rb + tc + 1];
+          e1 = t < T.tt ? e1 : e0;
+          const bool any = e1 > e0;
+          const int32_t* ci = any ? a.col_idx + e0 : reinterpret_cast<const int32_t*>(a.zsink);
+          const float* wi = any ? a.weight + e0 : reinterpret_cast<const float*>(a.zsink);
           ri.e0[u] = e0;
           ri.e1[u] = e1;
-          ri.k0[u] = e1 > e0 ? a.col_idx[e0] : 0;
-          ri.w0[u] = e1 > e0 ? a.weight[e0] : 0.f;
+          ri.k0[u] = *ci;
+          ri.w0[u] = *wi;
         }
       }
     };
@@ -310,22 +322,21 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       }
       return pair_group(a, lmap, a.src[ftile.kv], ftile.l, ftile.b, c * 8 + g).p;
     };
-    auto fetch_issue = [&](const bf16_t* gp, Raw& R) {
+    // `more` false: there is no such chunk; the loads still issue (from the
+    // zero sink), so every step issues the same loads.
+    auto fetch_issue = [&](const bf16_t* gp, Raw& R, bool more) {
       if (!IDENT) R.ri = fri;
       PairGroup pg;
       pg.p = gp;
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
         const int t = ftile.t0 + tid / 8 + 32 * u;  // identity: source token = t
-        const bool any = IDENT ? t < ftile.tt : fri.e1[u] > fri.e0[u];
-        if (any) {
-          const bf16_t* p = pg.p + (IDENT ? t : fri.k0[u]) * a.ss.t;
-          R.x0[u] = *reinterpret_cast<const uint4*>(p);
-          R.x1[u] = *reinterpret_cast<const uint4*>(p + a.ds / 2);
-        } else {
-          R.x0[u] = make_uint4(0, 0, 0, 0);
-          R.x1[u] = make_uint4(0, 0, 0, 0);
-        }
+        const bool any = more && (IDENT ? t < ftile.tt : fri.e1[u] > fri.e0[u]);
+        // a unit without data reads zeros from the sink: the loads stay
+        // unconditional, so the compiler can count them exactly
+        const bf16_t* p = any ? pg.p + (IDENT ? t : fri.k0[u]) * a.ss.t : a.zsink;
+        R.x0[u] = *reinterpret_cast<const uint4*>(p);
+        R.x1[u] = *reinterpret_cast<const uint4*>(p + a.ds / 2);
       }
     };
 
@@ -430,38 +441,46 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // chunk cs is consumed at step s(cs) = (cs / nch) * spt + cs % nch and
     // written into buffer s(cs) % 2 during the step before.
     auto step_of = [&](int cs) { return (cs / nch) * spt + cs % nch; };
-    fetch_issue(fetch_addr(0), rA);
-    if (nchunks > 1) fetch_issue(fetch_addr(1), rB);
+    fetch_issue(fetch_addr(0), rA, true);
+    fetch_issue(fetch_addr(nchunks > 1 ? 1 : 0), rB, nchunks > 1);
     {
-      const bf16_t* gp = nchunks > 2 ? fetch_addr(2) : nullptr;
+      const bf16_t* gp = fetch_addr(nchunks > 2 ? 2 : 0);
       transform(0, rA, lds, lds + kPlane);
-      if (nchunks > 2) fetch_issue(gp, rA);
+      fetch_issue(gp, rA, nchunks > 2);
     }
     lds_barrier();
-    int next = 1;  // next chunk to transform
-    for (int s = 0; s < nsteps; ++s) {
-      if (next < nchunks && step_of(next) == s + 1) {
-        bf16_t* buf = lds + ((s + 1) % 2) * 2 * kPlane;
-        const bool more = next + 2 < nchunks;
-        const bf16_t* gp = more ? fetch_addr(next + 2) : nullptr;
-        if (next & 1) {
-          transform(next, rB, buf, buf + kPlane);
-          if (more) fetch_issue(gp, rB);
-        } else {
-          transform(next, rA, buf, buf + kPlane);
-          if (more) fetch_issue(gp, rA);
-        }
-        ++next;
-      }
+    // Step s ends with a barrier; in an epilogue step (s % spt == nch) the
+    // consumers have staged the finished tile in buffer s % 2 at its middle
+    // barrier and the producers then write its rows (the consumers issue no
+    // global stores, so their weight loads never wait behind stores).
+    int s = 0;
+    auto end_step = [&]() {
       if (s % spt == nch) {
-        // epilogue step: the consumers staged the finished tile in buffer
-        // s % 2; write its rows (the consumers issue no global stores, so
-        // their weight loads never wait behind store completion)
         lds_barrier();
         store_rows(a, decode_tile(a, tbeg + s / spt), lds + (s % 2) * 2 * kPlane, tid);
       }
       lds_barrier();
+      ++s;
+    };
+    // Transform chunk `next` (consumed at step step_of(next)) during the step
+    // before it, from raw set R, and refill R with chunk next + 2.  Called
+    // alternately with rB and rA, so each set keeps its registers.
+    auto produce = [&](int next, Raw& R) {
+      while (s + 1 < step_of(next)) end_step();  // steps with nothing to transform
+      bf16_t* buf = lds + ((s + 1) % 2) * 2 * kPlane;
+      const bool more = next + 2 < nchunks;
+      const bf16_t* gp = fetch_addr(more ? next + 2 : next);
+      transform(next, R, buf, buf + kPlane);
+      fetch_issue(gp, R, more);
+      end_step();
+    };
+    int next = 1;
+    for (; next + 1 < nchunks; next += 2) {
+      produce(next, rB);
+      produce(next + 1, rA);
     }
+    if (next < nchunks) produce(next, rB);
+    while (s < nsteps) end_step();
     return;
   }
 
@@ -572,7 +591,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
 
   Tile T = decode_tile(a, tbeg);
   Blocks B = blocks(T, cw);
-  if (B.on) load_w(B, 0);
+  load_w(B, 0);  // valid addresses even for a pair block past dout
   lds_barrier();
   int cs = 0;  // global chunk index
   for (int s = 0; s < nsteps; ++s) {
@@ -589,6 +608,23 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
             for (int v = 0; v < 16; ++v) acc[m][p][v] = 0.f;
       }
       const bool computed = T.kv == 0 || !IDENT;
+      // weights of the next chunk (possibly of the next tile): fragment ks is
+      // reloaded as soon as the MFMAs of k-step ks have issued, so each load
+      // has about one step to arrive
+      Blocks Bn = B;
+      int cn = 0;
+      const bool more = cs + 1 < nchunks;
+      if (more) {
+        cn = (cs + 1) % nch;
+        if (cn == 0) Bn = blocks(decode_tile(a, tbeg + (cs + 1) / nch), cw);
+      }
+      // unconditional (past the last chunk, or for a pair block past dout, the
+      // addresses are still valid fragments): the compiler then counts the
+      // outstanding loads exactly instead of draining them all
+      auto reload = [&](int ks) {
+        wf[ks][0] = Bn.w0p[(cn * 8 + ks) * 64];
+        wf[ks][1] = Bn.w1p[(cn * 8 + ks) * 64];
+      };
       if (B.on) {
         const bf16_t* hi = buf;
         const bf16_t* lo = buf + kPlane;
@@ -613,6 +649,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
               acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w0, zc[m], acc[m][0], 0, 0, 0);
               acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w1, zc[m], acc[m][1], 0, 0, 0);
             }
+            reload(ks);
 #pragma unroll
             for (int m = 0; m < 4; ++m) zc[m] = zn[m];
           }
@@ -645,17 +682,13 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
                     __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][1], zh[m], acc[m][1], 0, 0, 0);
               }
             }
+            reload(ks);
           }
         }
+      } else {
+        load_w(Bn, cn);
       }
       ++cs;
-      // weights of the next chunk (possibly of the next tile)
-      if (cs < nchunks) {
-        const int cn = cs % nch;
-        Blocks Bn = B;
-        if (cn == 0) Bn = blocks(decode_tile(a, tbeg + cs / nch), cw);
-        if (Bn.on) load_w(Bn, cn);
-      }
       lds_barrier();
     } else {
       // ---------------- epilogue step ----------------

@@ -52,6 +52,11 @@ struct kvx_plan {
   void* w[2] = {nullptr, nullptr};  // tiled: [Lt][dout][din]; fused: packed fragments
   void* wh[2] = {nullptr, nullptr}; // fused, precision F16: packed fp16 fragments
   float* bias[2] = {nullptr, nullptr};
+  // fused kernel: a zero area that lanes without data load from, and an area
+  // that lanes without a valid output row store to (never read), so that
+  // every global access of the kernel is unconditional
+  void* zsink = nullptr;
+  void* trash = nullptr;
   void* block = nullptr;         // single allocation backing all of the above
 };
 
@@ -173,7 +178,8 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   size_t off_b0 = off_h1 + align256(hbytes);
   size_t off_b1 = off_b0 + align256(bbytes), off_m = off_b1 + align256(bbytes);
   size_t off_fs = off_m + align256(mbytes), off_ft = off_fs + align256(fsb);
-  size_t total = off_ft + align256(ftb);
+  size_t off_sink = off_ft + align256(ftb);
+  size_t total = off_sink + 2 * kSinkBytes;
   e = hipMalloc(&p->block, total);
   if (e != hipSuccess) return fail(hip_fail(e));
   p->bytes = static_cast<int64_t>(total);
@@ -189,6 +195,10 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   p->layer_map = reinterpret_cast<int32_t*>(base + off_m);
   p->fs = reinterpret_cast<double*>(base + off_fs);
   p->ft = reinterpret_cast<double*>(base + off_ft);
+  p->zsink = base + off_sink;
+  p->trash = base + off_sink + kSinkBytes;
+  e = hipMemset(p->zsink, 0, kSinkBytes);
+  if (e != hipSuccess) return fail(hip_fail(e));
 
   // Weights: copy to the host, repack, upload.  Plan creation is once per
   // translator, so clarity wins over speed here.
@@ -438,6 +448,8 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       a.lt = static_cast<int32_t>(Lt);
       a.fs = p->fs;
       a.ft = p->ft;
+      a.zsink = static_cast<const bf16_t*>(p->zsink);
+      a.trash = static_cast<bf16_t*>(p->trash);
       a.row_ptr = io.row_ptr;
       a.col_idx = io.col_idx;
       a.weight = io.weight;
