@@ -44,6 +44,10 @@
 
 namespace kvx {
 
+// Lambdas in kernels must be inlined: an outlined call spills its captured
+// state to the stack.
+#define KVX_INLINE __attribute__((always_inline))
+
 constexpr int kMT = 128;         // target rows per tile
 constexpr int kNT = 256;         // output features per tile (4 pair blocks)
 constexpr int kThreads = 512;    // 4 producer + 4 consumer waves
@@ -271,7 +275,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // =========================== producers ===========================
     const int g = tid % 8;  // 8-pair group within a chunk
 
-    auto row_info = [&](const Tile& T, RowInfo& ri) {
+    auto row_info = [&](const Tile& T, RowInfo& ri) KVX_INLINE {
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
         const int t = T.t0 + tid / 8 + 32 * u;
@@ -312,7 +316,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // Address of chunk cs's first 8-pair group for this thread (and the tile's
     // row info).  Done before the step's LDS writes: its LDS and scalar
     // lookups then do not wait for those writes to drain.
-    auto fetch_addr = [&](int cs) -> const bf16_t* {
+    auto fetch_addr = [&](int cs) KVX_INLINE -> const bf16_t* {
       const int tau = tbeg + cs / nch;
       const int c = cs % nch;
       if (tau != f_tile) {
@@ -324,7 +328,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     };
     // `more` false: there is no such chunk; the loads still issue (from the
     // zero sink), so every step issues the same loads.
-    auto fetch_issue = [&](const bf16_t* gp, Raw& R, bool more) {
+    auto fetch_issue = [&](const bf16_t* gp, Raw& R, bool more) KVX_INLINE {
       if (!IDENT) R.ri = fri;
       PairGroup pg;
       pg.p = gp;
@@ -342,7 +346,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
 
     float csc[CS_CACHE ? kUnits : 1][8], css[CS_CACHE ? kUnits : 1][8];
 
-    auto transform = [&](int cs, const Raw& R, bf16_t* hi, bf16_t* lo) {
+    auto transform = [&](int cs, const Raw& R, bf16_t* hi, bf16_t* lo) KVX_INLINE {
       const int tau = tbeg + cs / nch;
       const int c = cs % nch;
       const Tile T = decode_tile(a, tau);
@@ -440,7 +444,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
 
     // chunk cs is consumed at step s(cs) = (cs / nch) * spt + cs % nch and
     // written into buffer s(cs) % 2 during the step before.
-    auto step_of = [&](int cs) { return (cs / nch) * spt + cs % nch; };
+    auto step_of = [&](int cs) KVX_INLINE { return (cs / nch) * spt + cs % nch; };
     fetch_issue(fetch_addr(0), rA, true);
     fetch_issue(fetch_addr(nchunks > 1 ? 1 : 0), rB, nchunks > 1);
     {
@@ -454,7 +458,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // barrier and the producers then write its rows (the consumers issue no
     // global stores, so their weight loads never wait behind stores).
     int s = 0;
-    auto end_step = [&]() {
+    auto end_step = [&]() KVX_INLINE {
       if (s % spt == nch) {
         lds_barrier();
         store_rows(a, decode_tile(a, tbeg + s / spt), lds + (s % 2) * 2 * kPlane, tid);
@@ -465,7 +469,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // Transform chunk `next` (consumed at step step_of(next)) during the step
     // before it, from raw set R, and refill R with chunk next + 2.  Called
     // alternately with rB and rA, so each set keeps its registers.
-    auto produce = [&](int next, Raw& R) {
+    auto produce = [&](int next, Raw& R) KVX_INLINE {
       while (s + 1 < step_of(next)) end_step();  // steps with nothing to transform
       bf16_t* buf = lds + ((s + 1) % 2) * 2 * kPlane;
       const bool more = next + 2 < nchunks;
@@ -502,7 +506,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     const bf16x8* w0p;
     const bf16x8* w1p;
   };
-  auto blocks = [&](const Tile& T, int w) {
+  auto blocks = [&](const Tile& T, int w) KVX_INLINE {
     Blocks B;
     const int pb = T.nt * 4 + w;
     B.on = pb < npb;
@@ -519,7 +523,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
 
   f32x16 acc[4][2];
   bf16x8 wf[8][2];
-  auto load_w = [&](const Blocks& B, int c) {
+  auto load_w = [&](const Blocks& B, int c) KVX_INLINE {
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       wf[ks][0] = B.w0p[(c * 8 + ks) * 64];
@@ -532,7 +536,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   // 8*(v/4) + 4*(lane/32) + v%4 (v < 16) of blocks c0 and c1; staged at
   // column cw*64 + p*32 + feature offset.  Bias and frequencies come from
   // wave-uniform scalar loads (read-only data).
-  auto stage = [&](const Tile& Tc, const Blocks& B, bf16_t* st) {
+  auto stage = [&](const Tile& Tc, const Blocks& B, bf16_t* st) KVX_INLINE {
     typedef const __attribute__((address_space(4))) float* cfloat_p;
     typedef const __attribute__((address_space(4))) double* cdouble_p;
     const int l_u = __builtin_amdgcn_readfirstlane(Tc.l);
@@ -621,7 +625,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       // unconditional (past the last chunk, or for a pair block past dout, the
       // addresses are still valid fragments): the compiler then counts the
       // outstanding loads exactly instead of draining them all
-      auto reload = [&](int ks) {
+      auto reload = [&](int ks) KVX_INLINE {
         wf[ks][0] = Bn.w0p[(cn * 8 + ks) * 64];
         wf[ks][1] = Bn.w1p[(cn * 8 + ks) * 64];
       };
