@@ -135,6 +135,32 @@ __device__ __forceinline__ void unpack8(const uint4 v, float* x) {
 }
 
 typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Streaming (non-temporal) 16-byte load and store: source KV rows are read
+// once and target rows written once, so they should not displace the
+// translator weights, which every tile of a layer re-reads, from the L2.
+__device__ __forceinline__ uint4 ld_stream(const bf16_t* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+// Source row load: streaming when every source row is read by one tile only
+// (one N tile), cached when several N tiles re-read it.
+template <bool STREAM>
+__device__ __forceinline__ uint4 ld_src(const bf16_t* p) {
+  if constexpr (STREAM)
+    return ld_stream(p);
+  else
+    return *reinterpret_cast<const uint4*>(p);
+}
+__device__ __forceinline__ void st_stream(bf16_t* p, const uint4 v) {
+  u32x4 w;
+  w.x = v.x;
+  w.y = v.y;
+  w.z = v.z;
+  w.w = v.w;
+  __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(p));
+}
 
 // Round 8 floats to bf16 (hardware round-to-nearest-even) and pack.
 __device__ __forceinline__ uint4 pack8(const float* z) {
@@ -225,7 +251,7 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
     const int d = colg % a.dt;
     bf16_t* q = dst + hd * a.ts.h + t * a.ts.t + d;
     q = (t < Tc.tt && pbw < npb) ? q : a.trash;
-    *reinterpret_cast<uint4*>(q) = *reinterpret_cast<const uint4*>(st + r * LDO + sc8 * 8);
+    st_stream(q, *reinterpret_cast<const uint4*>(st + r * LDO + sc8 * 8));
   }
 }
 
@@ -249,7 +275,10 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
 // identity alignment V is already bf16 and goes through unchanged, except in
 // kF16 where every operand is fp16 (bf16 -> fp16 is exact in fp16's normal
 // range) so the consumers run a single contraction type.
-template <bool IDENT, bool CS_CACHE, int PREC>
+//
+// STREAM: source rows are read with streaming loads (one N tile, so no tile
+// re-reads them).
+template <bool IDENT, bool CS_CACHE, int PREC, bool STREAM>
 __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[fused_lds_bytes() / 2];
   // layer map and source RoPE frequencies: per-lane lookups go to LDS, so no
@@ -339,8 +368,8 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         // a unit without data reads zeros from the sink: the loads stay
         // unconditional, so the compiler can count them exactly
         const bf16_t* p = any ? pg.p + (IDENT ? t : fri.k0[u]) * a.ss.t : a.zsink;
-        R.x0[u] = *reinterpret_cast<const uint4*>(p);
-        R.x1[u] = *reinterpret_cast<const uint4*>(p + a.ds / 2);
+        R.x0[u] = ld_src<STREAM>(p);
+        R.x1[u] = ld_src<STREAM>(p + a.ds / 2);
       }
     };
 
@@ -408,8 +437,8 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
             const float w = a.weight[e];
             const bf16_t* p = pg.p + k * a.ss.t;
             float x0[8], x1[8];
-            unpack8(*reinterpret_cast<const uint4*>(p), x0);
-            unpack8(*reinterpret_cast<const uint4*>(p + a.ds / 2), x1);
+            unpack8(ld_src<STREAM>(p), x0);
+            unpack8(ld_src<STREAM>(p + a.ds / 2), x1);
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
               float y0 = x0[i], y1 = x1[i];

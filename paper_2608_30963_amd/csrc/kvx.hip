@@ -290,14 +290,24 @@ kvx_status kvx_plan_query(const kvx_plan* p, kvx_plan_info* info) {
 
 namespace {
 
+template <int PREC, bool STREAM>
+void launch_fused_ps(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
+  if (identity && ds128)
+    fused_kernel<true, true, PREC, STREAM><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  else if (identity)
+    fused_kernel<true, false, PREC, STREAM><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  else
+    fused_kernel<false, false, PREC, STREAM><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+}
+
+// Streaming source loads when a single N tile covers the output (no tile
+// re-reads a source row); cached loads otherwise.
 template <int PREC>
 void launch_fused_p(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
-  if (identity && ds128)
-    fused_kernel<true, true, PREC><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
-  else if (identity)
-    fused_kernel<true, false, PREC><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  if (a.n_tiles == 1)
+    launch_fused_ps<PREC, true>(identity, ds128, grid, st, a);
   else
-    fused_kernel<false, false, PREC><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+    launch_fused_ps<PREC, false>(identity, ds128, grid, st, a);
 }
 
 void launch_fused(bool identity, bool ds128, int precision, int grid, hipStream_t st,
