@@ -66,13 +66,14 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def recorded_traffic(workload: str, precision: str, src_tokens: int, batch: int):
+def recorded_traffic(workload: str, precision: str, src_tokens: int, batch: int, layout: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary of
     this workload (FETCH_SIZE and WRITE_SIZE, scaled by a copy kernel's
     reading), or None when no summary matches or the kernel sources have
     changed since the counters were taken."""
     want = {"workload": workload, "precision": precision, "src_tokens": str(src_tokens),
-            "batch": str(batch), "kernel_source_sha256": kernel_source_hash()}
+            "batch": str(batch), "target_layout": layout,
+            "kernel_source_sha256": kernel_source_hash()}
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
         rec = {}
         with open(path) as fh:
@@ -129,6 +130,9 @@ def main():
     ap.add_argument("--batch", type=int, default=None, help="override contexts per call")
     ap.add_argument("--sets", type=int, default=3, help="rotating buffer sets")
     ap.add_argument("--precision", choices=["bf16x2", "bf16", "f16"], default="bf16x2")
+    ap.add_argument("--paged", type=int, default=0, metavar="BLOCK",
+                    help="write a paged target cache with BLOCK tokens per block through a "
+                         "shuffled block table (0 = contiguous target layout)")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--no-cpu", action="store_true")
@@ -180,6 +184,22 @@ def main():
     cap = prob.tgt_capacity
     tdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
     oshape = (spec.tgt.n_layers, spec.batch, spec.tgt.n_kv_heads, cap, spec.tgt.head_dim)
+    bt_dev, paging = None, {}
+    if args.paged > 0:
+        # every context's logical blocks on distinct, shuffled physical blocks
+        bs = args.paged
+        need = [(int(t) + bs - 1) // bs for t in prob.tgt_tokens]
+        nblk = sum(need)
+        perm = np.random.default_rng(0).permutation(nblk).astype(np.int32)
+        table = np.zeros((spec.batch, max(need)), dtype=np.int32)
+        k = 0
+        for b, n in enumerate(need):
+            table[b, :n] = perm[k:k + n]
+            k += n
+        bt_dev = torch.from_numpy(table).cuda()
+        oshape = (spec.tgt.n_layers, nblk, spec.tgt.n_kv_heads, bs, spec.tgt.head_dim)
+        paging = {"block_table": bt_dev, "block_size": bs, "max_blocks": table.shape[1],
+                  "num_blocks": nblk}
     sk0, sv0 = dev(prob.src_k), dev(prob.src_v)
     sets = []
     for i in range(max(1, args.sets)):
@@ -191,7 +211,7 @@ def main():
     tt = None if ident else prob.tgt_tokens
     stream = torch.cuda.current_stream()
     ios = [kvx.make_io(spec.batch, spec.src_tokens, s[0], s[1], s[2], s[3], cap, tt, rp, ci,
-                       wt) for s in sets]
+                       wt, **paging) for s in sets]
 
     def step(i):
         kvx.kvx_translate(tr.plan, ios[i % len(ios)][0], stream)
@@ -238,12 +258,19 @@ def main():
     for i in range(len(sets)):
         step(i)
     torch.cuda.synchronize()
-    for b in range(spec.batch):
-        t_b = int(prob.tgt_tokens[b])
-        for s in sets:
-            if torch.isnan(s[2][:, b, :, :t_b]).any() or torch.isnan(s[3][:, b, :, :t_b]).any():
-                print("bench.py: output has unwritten rows", file=sys.stderr)
-                sys.exit(1)
+    for s in sets:
+        if args.paged > 0:  # every block of the table is fully used except tails
+            unwritten = int(torch.isnan(s[2]).sum() + torch.isnan(s[3]).sum())
+            tail = sum(-int(t) % args.paged for t in prob.tgt_tokens)
+            bad = unwritten != 2 * tail * spec.tgt.n_layers * spec.tgt.n_kv_heads * \
+                spec.tgt.head_dim
+        else:
+            bad = any(torch.isnan(s[2][:, b, :, :int(t)]).any() or
+                      torch.isnan(s[3][:, b, :, :int(t)]).any()
+                      for b, t in enumerate(prob.tgt_tokens))
+        if bad:
+            print("bench.py: output has unwritten rows", file=sys.stderr)
+            sys.exit(1)
 
     tokens = spec.batch * spec.src_tokens
     value = tokens / (ms * 1e-3)
@@ -252,7 +279,8 @@ def main():
     gbs = alg["bytes"] / (ms_kernel * 1e-3) / 1e9
     tfs = alg["flops"] / (ms_kernel * 1e-3) / 1e12
     kernel_name = "fused_kernel" if info.kernel == 1 else "tiled_kernel"
-    traffic = recorded_traffic(spec.name, args.precision, spec.src_tokens, spec.batch)
+    layout = f"paged, {args.paged}-token blocks" if args.paged else "contiguous"
+    traffic = recorded_traffic(spec.name, args.precision, spec.src_tokens, spec.batch, layout)
     roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kernel_name,
             "bytes_per_launch": alg["bytes"], "ms_per_launch": round(ms_kernel, 5),
@@ -275,6 +303,7 @@ def main():
                    "src_heads": f"{spec.src.n_kv_heads}x{spec.src.head_dim}",
                    "tgt_heads": f"{spec.tgt.n_kv_heads}x{spec.tgt.head_dim}",
                    "mix": spec.mix, "precision": args.precision,
+                   "target_layout": layout,
                    "parallelism": "single GPU"},
         "ms_per_handoff": round(ms, 5) if spec.batch == 1 else None,
         "ms_wall_per_step": round(ms_wall, 5),

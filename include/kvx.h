@@ -110,6 +110,20 @@ typedef struct {
   void* tgt_v;
   int64_t tgt_stride[4];
   int32_t tgt_capacity;      /* >= max_b T_t[b]; rows t >= T_t[b] are left untouched */
+  /* Paged target layout (optional; the cache assembly of a serving system
+   * that pages its KV memory, Section 2.2 and Section 6.1).  block_table ==
+   * NULL: the contiguous layout above.  Otherwise target token t of context b
+   * is written to physical block block_table[b * max_blocks + t / block_size]
+   * at slot t % block_size: tgt_stride then reads (layer, block, head, slot),
+   * and all-zero strides mean [Lt][num_blocks][Ht][block_size][Dt].
+   * tgt_capacity is not used; T_t[b] <= max_blocks * block_size is required.
+   * Blocks and slots that no target token maps to are left untouched.  Block
+   * ids are trusted unless KVX_VALIDATE=1 (then 0 <= id < num_blocks is
+   * checked for every entry a target token uses; KVX_EDATA otherwise). */
+  const int32_t* block_table; /* device [B][max_blocks] */
+  int32_t block_size;         /* tokens per block, > 0 */
+  int32_t max_blocks;         /* block_table entries per context, > 0 */
+  int32_t num_blocks;         /* physical blocks in tgt_k / tgt_v, > 0 */
 } kvx_io;
 
 typedef struct kvx_plan kvx_plan;

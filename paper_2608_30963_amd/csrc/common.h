@@ -26,6 +26,26 @@ struct Strides {
   int64_t l, b, h, t;  // elements; head_dim is unit-stride
 };
 
+// Optional paged target layout (a block table in the manner of paged KV
+// caches): target token t of context b is stored in physical block
+// table[b * max_blocks + t / block_size] at slot t % block_size; the target
+// strides' batch entry is then the block stride and their token entry the
+// slot stride.  table == nullptr: the contiguous layout.
+struct Paging {
+  const int32_t* table;  // device, this launch's contexts
+  int32_t block_size;
+  int32_t max_blocks;
+};
+
+// Element offset of target row (context b, token t), layer and head excluded,
+// given the row's physical block (ignored without paging).
+__device__ __forceinline__ int64_t target_row(const Paging& pg, const Strides& ts, int b, int t,
+                                              int32_t block) {
+  return pg.table ? static_cast<int64_t>(block) * ts.b +
+                        static_cast<int64_t>(t % pg.block_size) * ts.t
+                  : static_cast<int64_t>(b) * ts.b + static_cast<int64_t>(t) * ts.t;
+}
+
 // Exact widening of a bfloat16 bit pattern.
 __device__ __forceinline__ float bf16_to_f32(bf16_t h) {
   return __uint_as_float(static_cast<uint32_t>(h) << 16);

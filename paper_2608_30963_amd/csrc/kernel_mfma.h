@@ -76,6 +76,7 @@ struct FusedArgs {
   int32_t total_tiles;      // row_tiles * n_tiles * 2 * Lt
   const bf16_t* zsink;      // kSinkBytes of zeros: source of lanes without data
   bf16_t* trash;            // kSinkBytes never read: target of lanes without a row
+  Paging pg;                // optional paged target layout
   BatchArgs ba;
 };
 
@@ -225,17 +226,38 @@ struct RowInfo {
   float w0[kUnits];
 };
 
+// Store pieces per producer thread and tile: the rows of thread `it` are
+// it / 32 + 8 i, i < kRowsPerThread.
+constexpr int kRowsPerThread = kMT * kNT / 8 / 256;
+
+// Physical blocks of this thread's rows of tile Tc (paged layout), loaded a
+// tile ahead of the stores (unconditional loads: rows past the context's end
+// read the last row's entry).
+template <bool PAGED>
+__device__ __forceinline__ void load_blocks(const FusedArgs& a, const Tile& Tc, int it,
+                                            int32_t (&blk)[kRowsPerThread]) {
+  if constexpr (PAGED) {
+#pragma unroll
+    for (int i = 0; i < kRowsPerThread; ++i) {
+      const int t = Tc.t0 + it / 32 + 8 * i;
+      const int tc = t < Tc.tt ? t : Tc.tt - 1;
+      blk[i] = a.pg.table[Tc.b * a.pg.max_blocks + tc / a.pg.block_size];
+    }
+  }
+}
+
 // Whole 16-byte pieces of target rows from the staging buffer [token][kNT+8]
 // of tile Tc (staged column w*64 + p*32 + j holds feature c_p + j of pair
 // block 4*nt + w); thread `it` of 256.
+template <bool PAGED>
 __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, const bf16_t* st,
-                                           int it) {
+                                           int it, const int32_t (&blk)[kRowsPerThread]) {
   constexpr int LDO = kNT + 8;
   const int npb = a.dout / 64;
   const int per_head = a.dt / 64;
-  bf16_t* dst = a.tgt[Tc.kv] + Tc.l * a.ts.l + Tc.b * a.ts.b;
-#pragma unroll 4
-  for (int i = 0; i < kMT * kNT / 8 / 256; ++i) {
+  bf16_t* dst = a.tgt[Tc.kv] + Tc.l * a.ts.l;
+#pragma unroll
+  for (int i = 0; i < kRowsPerThread; ++i) {
     const int pc = it + 256 * i;
     const int r = pc / (kNT / 8);
     const int sc8 = pc % (kNT / 8);   // staged column / 8
@@ -249,7 +271,10 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
     const int colg = hpw * a.dt + 32 * (pbw % per_head) + half * (a.dt / 2) + (sc8 % 4) * 8;
     const int hd = colg / a.dt;
     const int d = colg % a.dt;
-    bf16_t* q = dst + hd * a.ts.h + t * a.ts.t + d;
+    const int64_t row = PAGED ? static_cast<int64_t>(blk[i]) * a.ts.b +
+                                    static_cast<int64_t>(t % a.pg.block_size) * a.ts.t
+                              : static_cast<int64_t>(Tc.b) * a.ts.b + static_cast<int64_t>(t) * a.ts.t;
+    bf16_t* q = dst + hd * a.ts.h + row + d;
     q = (t < Tc.tt && pbw < npb) ? q : a.trash;
     st_stream(q, *reinterpret_cast<const uint4*>(st + r * LDO + sc8 * 8));
   }
@@ -277,8 +302,8 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
 // range) so the consumers run a single contraction type.
 //
 // STREAM: source rows are read with streaming loads (one N tile, so no tile
-// re-reads them).
-template <bool IDENT, bool CS_CACHE, int PREC, bool STREAM>
+// re-reads them).  PAGED: target rows go through the block table.
+template <bool IDENT, bool CS_CACHE, int PREC, bool STREAM, bool PAGED>
 __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[fused_lds_bytes() / 2];
   // layer map and source RoPE frequencies: per-lane lookups go to LDS, so no
@@ -487,10 +512,15 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // barrier and the producers then write its rows (the consumers issue no
     // global stores, so their weight loads never wait behind stores).
     int s = 0;
+    // physical blocks of this thread's rows of the next tile to be stored
+    int32_t blk[kRowsPerThread];
+    load_blocks<PAGED>(a, decode_tile(a, tbeg), tid, blk);
     auto end_step = [&]() KVX_INLINE {
       if (s % spt == nch) {
         lds_barrier();
-        store_rows(a, decode_tile(a, tbeg + s / spt), lds + (s % 2) * 2 * kPlane, tid);
+        const int tau = tbeg + s / spt;
+        store_rows<PAGED>(a, decode_tile(a, tau), lds + (s % 2) * 2 * kPlane, tid, blk);
+        load_blocks<PAGED>(a, decode_tile(a, tau + 1 < tend ? tau + 1 : tau), tid, blk);
       }
       lds_barrier();
       ++s;

@@ -32,6 +32,7 @@ struct TiledArgs {
   const float* weight;
   int32_t identity;
   int32_t rows;             // target rows per tile
+  Paging pg;                // optional paged target layout
   BatchArgs ba;
 };
 
@@ -93,7 +94,7 @@ __global__ void __launch_bounds__(256) tiled_kernel(TiledArgs<T> a) {
   const int ht2 = a.dt / 2;
   const T* wl = a.w[kv] + static_cast<int64_t>(l) * a.dout * a.din;
   const float* bl = a.bias[kv] + static_cast<int64_t>(l) * a.dout;
-  T* dst = a.tgt[kv] + l * a.ts.l + b * a.ts.b;
+  T* dst = a.tgt[kv] + l * a.ts.l;
   const int n_out = nrows * a.ht * ht2;
   for (int it = threadIdx.x; it < n_out; it += blockDim.x) {
     int i = it % ht2;
@@ -120,7 +121,8 @@ __global__ void __launch_bounds__(256) tiled_kernel(TiledArgs<T> a) {
       u0 = y0;
       u1 = y1;
     }
-    T* p = dst + h * a.ts.h + t * a.ts.t;
+    const int32_t blk = a.pg.table ? a.pg.table[b * a.pg.max_blocks + t / a.pg.block_size] : 0;
+    T* p = dst + h * a.ts.h + target_row(a.pg, a.ts, b, t, blk);
     p[i] = store_cvt<T>(u0);
     p[i + ht2] = store_cvt<T>(u1);
   }

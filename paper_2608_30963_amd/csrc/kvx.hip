@@ -290,14 +290,22 @@ kvx_status kvx_plan_query(const kvx_plan* p, kvx_plan_info* info) {
 
 namespace {
 
+template <int PREC, bool STREAM, bool PAGED>
+void launch_fused_psp(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
+  if (identity && ds128)
+    fused_kernel<true, true, PREC, STREAM, PAGED><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  else if (identity)
+    fused_kernel<true, false, PREC, STREAM, PAGED><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  else
+    fused_kernel<false, false, PREC, STREAM, PAGED><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+}
+
 template <int PREC, bool STREAM>
 void launch_fused_ps(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
-  if (identity && ds128)
-    fused_kernel<true, true, PREC, STREAM><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
-  else if (identity)
-    fused_kernel<true, false, PREC, STREAM><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  if (a.pg.table)
+    launch_fused_psp<PREC, STREAM, true>(identity, ds128, grid, st, a);
   else
-    fused_kernel<false, false, PREC, STREAM><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+    launch_fused_psp<PREC, STREAM, false>(identity, ds128, grid, st, a);
 }
 
 // Streaming source loads when a single N tile covers the output (no tile
@@ -347,6 +355,23 @@ kvx_status validate_csr(const kvx_io& io, int64_t rows, hipStream_t st) {
   return KVX_OK;
 }
 
+// Host-side check of the block ids that target tokens use (validation mode).
+kvx_status validate_blocks(const kvx_io& io, const std::vector<int32_t>& ttok, hipStream_t st) {
+  std::vector<int32_t> bt(size_t(io.batch) * io.max_blocks);
+  hipError_t e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e);
+  e = hipMemcpy(bt.data(), io.block_table, bt.size() * sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  for (int b = 0; b < io.batch; ++b) {
+    const int64_t used = (int64_t(ttok[b]) + io.block_size - 1) / io.block_size;
+    for (int64_t j = 0; j < used; ++j) {
+      const int32_t id = bt[size_t(b) * io.max_blocks + j];
+      if (id < 0 || id >= io.num_blocks) return KVX_EDATA;
+    }
+  }
+  return KVX_OK;
+}
+
 }  // namespace
 
 extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void* stream) {
@@ -355,12 +380,17 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
   if (io.batch < 0 || io.src_tokens < 0 || io.tgt_capacity < 0) return KVX_EINVAL;
   if (io.batch == 0) return KVX_OK;
   const bool identity = io.tgt_tokens == nullptr;
+  const bool paged = io.block_table != nullptr;
+  if (paged && (io.block_size <= 0 || io.max_blocks <= 0 || io.num_blocks <= 0))
+    return KVX_EINVAL;
+  // rows a context may hold in the target layout
+  const int64_t cap = paged ? int64_t(io.max_blocks) * io.block_size : io.tgt_capacity;
   std::vector<int32_t> ttok(io.batch);
   int64_t rows = 0;
   for (int b = 0; b < io.batch; ++b) {
     const int32_t t = identity ? io.src_tokens : io.tgt_tokens[b];
     if (t < 0) return KVX_EINVAL;
-    if (t > io.tgt_capacity) return KVX_ESHAPE;
+    if (t > cap) return KVX_ESHAPE;
     ttok[b] = t;
     rows += t;
   }
@@ -380,15 +410,18 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
     io.src_stride[0] = B * io.src_stride[1];
   }
   if (all_zero(io.tgt_stride)) {
+    // contiguous [Lt][B][Ht][tgt_capacity][Dt], or paged
+    // [Lt][num_blocks][Ht][block_size][Dt]
     io.tgt_stride[3] = Dt;
-    io.tgt_stride[2] = Dt * int64_t(io.tgt_capacity);
+    io.tgt_stride[2] = Dt * (paged ? int64_t(io.block_size) : int64_t(io.tgt_capacity));
     io.tgt_stride[1] = Ht * io.tgt_stride[2];
-    io.tgt_stride[0] = B * io.tgt_stride[1];
+    io.tgt_stride[0] = (paged ? int64_t(io.num_blocks) : B) * io.tgt_stride[1];
   }
   for (int i = 0; i < 4; ++i)
     if (io.src_stride[i] < 0 || io.tgt_stride[i] < 0) return KVX_ESHAPE;
   // strides must keep one row (head_dim values) inside the next-outer step
-  if ((io.src_stride[3] < Ds && io.src_tokens > 1) || (io.tgt_stride[3] < Dt && io.tgt_capacity > 1))
+  const int64_t tgt_rows = paged ? io.block_size : io.tgt_capacity;  // rows per token stride run
+  if ((io.src_stride[3] < Ds && io.src_tokens > 1) || (io.tgt_stride[3] < Dt && tgt_rows > 1))
     return KVX_ESHAPE;
   (void)Ls;
 
@@ -396,6 +429,10 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
   const char* vmode = std::getenv("KVX_VALIDATE");
   if (!identity && vmode && vmode[0] == '1') {
     kvx_status s = validate_csr(io, rows, st);
+    if (s != KVX_OK) return s;
+  }
+  if (paged && vmode && vmode[0] == '1') {
+    kvx_status s = validate_blocks(io, ttok, st);
     if (s != KVX_OK) return s;
   }
 
@@ -431,8 +468,12 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
     if (tiles == 0) continue;
     const char* sk = static_cast<const char*>(io.src_k) + b0 * io.src_stride[1] * esz;
     const char* sv = static_cast<const char*>(io.src_v) + b0 * io.src_stride[1] * esz;
-    char* tk = static_cast<char*>(io.tgt_k) + b0 * io.tgt_stride[1] * esz;
-    char* tv = static_cast<char*>(io.tgt_v) + b0 * io.tgt_stride[1] * esz;
+    // paged: blocks are shared by all contexts; the table row moves instead
+    const int64_t toff = paged ? 0 : b0 * io.tgt_stride[1] * esz;
+    char* tk = static_cast<char*>(io.tgt_k) + toff;
+    char* tv = static_cast<char*>(io.tgt_v) + toff;
+    const Paging pg{paged ? io.block_table + b0 * io.max_blocks : nullptr,
+                    paged ? io.block_size : 1, paged ? io.max_blocks : 0};
     if (fused) {
       FusedArgs a{};
       a.src[0] = reinterpret_cast<const bf16_t*>(sk);
@@ -465,6 +506,7 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       a.weight = io.weight;
       a.n_tiles = (p->dout / 64 + 3) / 4;
       a.row_tiles = tiles;
+      a.pg = pg;
       a.ba = ba;
       const int64_t total = int64_t(tiles) * a.n_tiles * 2 * Lt;
       if (total > INT32_MAX) return KVX_ESHAPE;
@@ -489,7 +531,7 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
         a.hs = Hs; a.ds = Ds; a.ht = Ht; a.dt = Dt; a.din = p->din; a.dout = p->dout;
         a.fs = p->fs; a.ft = p->ft;
         a.row_ptr = io.row_ptr; a.col_idx = io.col_idx; a.weight = io.weight;
-        a.identity = identity; a.rows = rows_per_tile; a.ba = ba;
+        a.identity = identity; a.rows = rows_per_tile; a.pg = pg; a.ba = ba;
         tiled_kernel<float><<<dim3(tiles, Lt, 2), dim3(256), lds, st>>>(a);
       } else {
         TiledArgs<bf16_t> a{};
@@ -505,7 +547,7 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
         a.hs = Hs; a.ds = Ds; a.ht = Ht; a.dt = Dt; a.din = p->din; a.dout = p->dout;
         a.fs = p->fs; a.ft = p->ft;
         a.row_ptr = io.row_ptr; a.col_idx = io.col_idx; a.weight = io.weight;
-        a.identity = identity; a.rows = rows_per_tile; a.ba = ba;
+        a.identity = identity; a.rows = rows_per_tile; a.pg = pg; a.ba = ba;
         tiled_kernel<bf16_t><<<dim3(tiles, Lt, 2), dim3(256), lds, st>>>(a);
       }
     }

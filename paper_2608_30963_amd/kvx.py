@@ -51,7 +51,8 @@ class IO(C.Structure):
                 ("tgt_tokens", C.c_void_p), ("row_ptr", C.c_void_p),
                 ("col_idx", C.c_void_p), ("weight", C.c_void_p),
                 ("tgt_k", C.c_void_p), ("tgt_v", C.c_void_p), ("tgt_stride", C.c_int64 * 4),
-                ("tgt_capacity", C.c_int32)]
+                ("tgt_capacity", C.c_int32), ("block_table", C.c_void_p),
+                ("block_size", C.c_int32), ("max_blocks", C.c_int32), ("num_blocks", C.c_int32)]
 
 
 class PlanInfo(C.Structure):
@@ -143,8 +144,10 @@ def kvx_plan_create(src, tgt, mix: int, layer_map: Sequence[int], dtype: int, w_
 
 def make_io(batch: int, src_tokens: int, src_k, src_v, tgt_k, tgt_v, tgt_capacity: int,
             tgt_tokens=None, row_ptr=None, col_idx=None, weight=None,
-            src_stride=(0, 0, 0, 0), tgt_stride=(0, 0, 0, 0)):
-    """Build the kvx_io struct; returns (io, keepalive)."""
+            src_stride=(0, 0, 0, 0), tgt_stride=(0, 0, 0, 0), block_table=None,
+            block_size: int = 0, max_blocks: int = 0, num_blocks: int = 0):
+    """Build the kvx_io struct; returns (io, keepalive).  ``block_table``
+    (device int32 [batch][max_blocks]) selects the paged target layout."""
     keep = []
     tt = None
     if tgt_tokens is not None:
@@ -154,7 +157,8 @@ def make_io(batch: int, src_tokens: int, src_k, src_v, tgt_k, tgt_v, tgt_capacit
             (C.c_int64 * 4)(*[int(x) for x in src_stride]),
             C.cast(tt, C.c_void_p).value if tt is not None else None,
             _ptr(row_ptr), _ptr(col_idx), _ptr(weight), _ptr(tgt_k), _ptr(tgt_v),
-            (C.c_int64 * 4)(*[int(x) for x in tgt_stride]), int(tgt_capacity))
+            (C.c_int64 * 4)(*[int(x) for x in tgt_stride]), int(tgt_capacity),
+            _ptr(block_table), int(block_size), int(max_blocks), int(num_blocks))
     return io, keep
 
 
@@ -204,11 +208,21 @@ class Translator:
 
     def __call__(self, src_k, src_v, tgt_k, tgt_v, tgt_capacity=None, tgt_tokens=None,
                  row_ptr=None, col_idx=None, weight=None, stream=None,
-                 src_stride=(0, 0, 0, 0), tgt_stride=(0, 0, 0, 0)):
+                 src_stride=(0, 0, 0, 0), tgt_stride=(0, 0, 0, 0), block_table=None,
+                 block_size=0):
+        """Contiguous targets [Lt][B][Ht][cap][Dt]; with ``block_table``
+        ([B][max_blocks] int32 on the device) paged targets
+        [Lt][num_blocks][Ht][block_size][Dt] (or the given strides)."""
         batch, src_tokens = int(src_k.shape[1]), int(src_k.shape[3])
-        cap = int(tgt_k.shape[3]) if tgt_capacity is None else int(tgt_capacity)
+        max_blocks = num_blocks = 0
+        if block_table is not None:
+            max_blocks, num_blocks = int(block_table.shape[1]), int(tgt_k.shape[1])
+            cap = 0 if tgt_capacity is None else int(tgt_capacity)
+        else:
+            cap = int(tgt_k.shape[3]) if tgt_capacity is None else int(tgt_capacity)
         io, keep = make_io(batch, src_tokens, src_k, src_v, tgt_k, tgt_v, cap, tgt_tokens,
-                           row_ptr, col_idx, weight, src_stride, tgt_stride)
+                           row_ptr, col_idx, weight, src_stride, tgt_stride, block_table,
+                           block_size, max_blocks, num_blocks)
         kvx_translate(self.plan, io, stream)
         del keep
 
