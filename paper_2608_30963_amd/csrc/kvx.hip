@@ -12,6 +12,7 @@
 #include "kvx.h"
 #include "common.h"
 #include "kernel_mfma.h"
+#include "fused_launch.h"
 #include "kernel_tiled.h"
 
 using namespace kvx;
@@ -290,40 +291,12 @@ kvx_status kvx_plan_query(const kvx_plan* p, kvx_plan_info* info) {
 
 namespace {
 
-template <int PREC, bool STREAM, bool PAGED>
-void launch_fused_psp(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
-  if (identity && ds128)
-    fused_kernel<true, true, PREC, STREAM, PAGED><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
-  else if (identity)
-    fused_kernel<true, false, PREC, STREAM, PAGED><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
-  else
-    fused_kernel<false, false, PREC, STREAM, PAGED><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
-}
-
-template <int PREC, bool STREAM>
-void launch_fused_ps(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
-  if (a.pg.table)
-    launch_fused_psp<PREC, STREAM, true>(identity, ds128, grid, st, a);
-  else
-    launch_fused_psp<PREC, STREAM, false>(identity, ds128, grid, st, a);
-}
-
-// Streaming source loads when a single N tile covers the output (no tile
-// re-reads a source row); cached loads otherwise.
-template <int PREC>
-void launch_fused_p(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
-  if (a.n_tiles == 1)
-    launch_fused_ps<PREC, true>(identity, ds128, grid, st, a);
-  else
-    launch_fused_ps<PREC, false>(identity, ds128, grid, st, a);
-}
-
 void launch_fused(bool identity, bool ds128, int precision, int grid, hipStream_t st,
                   const FusedArgs& a) {
   switch (precision) {
-    case KVX_PREC_BF16: launch_fused_p<kBF16>(identity, ds128, grid, st, a); break;
-    case KVX_PREC_F16: launch_fused_p<kF16>(identity, ds128, grid, st, a); break;
-    default: launch_fused_p<kBF16X2>(identity, ds128, grid, st, a); break;
+    case KVX_PREC_BF16: launch_fused_bf16(identity, ds128, grid, st, a); break;
+    case KVX_PREC_F16: launch_fused_f16(identity, ds128, grid, st, a); break;
+    default: launch_fused_bf16x2(identity, ds128, grid, st, a); break;
   }
 }
 
