@@ -358,12 +358,15 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     };
 
     // Raw first-entry data of a chunk (global chunk index cs) and the row
-    // info it was fetched with; two such sets rotate (cs even / odd).
+    // info it was fetched with.  With identity alignment three sets rotate
+    // (cs mod 3), so two chunks stay in flight while one is transformed; the
+    // span-map path (more registers per set: alignment entries) uses two.
+    constexpr int kDepth = IDENT ? 3 : 2;
     struct Raw {
       uint4 x0[kUnits], x1[kUnits];
       RowInfo ri;
     };
-    Raw rA, rB;
+    Raw rA, rB, rC;
     int f_tile = -1;
     Tile ftile{};
     RowInfo fri;
@@ -501,10 +504,11 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     auto step_of = [&](int cs) KVX_INLINE { return (cs / nch) * spt + cs % nch; };
     fetch_issue(fetch_addr(0), rA, true);
     fetch_issue(fetch_addr(nchunks > 1 ? 1 : 0), rB, nchunks > 1);
+    if constexpr (kDepth == 3) fetch_issue(fetch_addr(nchunks > 2 ? 2 : 0), rC, nchunks > 2);
     {
-      const bf16_t* gp = fetch_addr(nchunks > 2 ? 2 : 0);
+      const bf16_t* gp = fetch_addr(nchunks > kDepth ? kDepth : 0);
       transform(0, rA, lds, lds + kPlane);
-      fetch_issue(gp, rA, nchunks > 2);
+      fetch_issue(gp, rA, nchunks > kDepth);
     }
     lds_barrier();
     // Step s ends with a barrier; in an epilogue step (s % spt == nch) the
@@ -526,23 +530,34 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       ++s;
     };
     // Transform chunk `next` (consumed at step step_of(next)) during the step
-    // before it, from raw set R, and refill R with chunk next + 2.  Called
-    // alternately with rB and rA, so each set keeps its registers.
+    // before it, from raw set R, and refill R with chunk next + kDepth.
+    // Called with the sets in turn (chunk mod kDepth), so each set keeps its
+    // registers.
     auto produce = [&](int next, Raw& R) KVX_INLINE {
       while (s + 1 < step_of(next)) end_step();  // steps with nothing to transform
       bf16_t* buf = lds + ((s + 1) % 2) * 2 * kPlane;
-      const bool more = next + 2 < nchunks;
-      const bf16_t* gp = fetch_addr(more ? next + 2 : next);
+      const bool more = next + kDepth < nchunks;
+      const bf16_t* gp = fetch_addr(more ? next + kDepth : next);
       transform(next, R, buf, buf + kPlane);
       fetch_issue(gp, R, more);
       end_step();
     };
     int next = 1;
-    for (; next + 1 < nchunks; next += 2) {
-      produce(next, rB);
-      produce(next + 1, rA);
+    if constexpr (kDepth == 3) {
+      for (; next + 2 < nchunks; next += 3) {
+        produce(next, rB);
+        produce(next + 1, rC);
+        produce(next + 2, rA);
+      }
+      if (next < nchunks) produce(next, rB);
+      if (next + 1 < nchunks) produce(next + 1, rC);
+    } else {
+      for (; next + 1 < nchunks; next += 2) {
+        produce(next, rB);
+        produce(next + 1, rA);
+      }
+      if (next < nchunks) produce(next, rB);
     }
-    if (next < nchunks) produce(next, rB);
     while (s < nsteps) end_step();
     return;
   }
