@@ -310,6 +310,11 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   // vector load inside the step loop can queue behind outstanding stores
   __shared__ int32_t lmap[kMaxLayerMap];
   __shared__ double fsl[kMaxHalfDim];
+  // target RoPE: theta_i / 2pi, and cos/sin of the rotation by 32 positions
+  __shared__ double ftl[kMaxHalfDim];
+  __shared__ float2 rot32[kMaxHalfDim];
+  // bias of the tile being finished, in staging-column order (tile parity)
+  __shared__ __attribute__((aligned(16))) float biasl[2][kNT];
 
   const int G = gridDim.x;
   const int wid = xcd_remap(blockIdx.x, G);
@@ -323,6 +328,12 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   const int tid = threadIdx.x;
   for (int i = tid; i < a.lt * a.mix; i += kThreads) lmap[i] = a.layer_map[i];
   for (int i = tid; i < a.ds / 2; i += kThreads) fsl[i] = a.fs[i];
+  for (int i = tid; i < a.dt / 2; i += kThreads) {
+    ftl[i] = a.ft[i];
+    float c, sn;
+    rope_cs(a.ft[i], 32, c, sn);
+    rot32[i] = make_float2(c, sn);
+  }
   __syncthreads();
 
   if (tid < kProducers) {
@@ -360,8 +371,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // Raw first-entry data of a chunk (global chunk index cs) and the row
     // info it was fetched with.  With identity alignment three sets rotate
     // (cs mod 3), so two chunks stay in flight while one is transformed; the
-    // span-map path (more registers per set: alignment entries) uses two.
-    constexpr int kDepth = IDENT ? 3 : 2;
+    // span-map path (more registers per set: alignment entries) and the paged
+    // path (block ids of the next tile) use two.
+    constexpr int kDepth = IDENT && !PAGED ? 3 : 2;
     struct Raw {
       uint4 x0[kUnits], x1[kUnits];
       RowInfo ri;
@@ -519,12 +531,30 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // physical blocks of this thread's rows of the next tile to be stored
     int32_t blk[kRowsPerThread];
     load_blocks<PAGED>(a, decode_tile(a, tbeg), tid, blk);
+    // Bias entry `tid` of a tile in staging-column order (consumer wave
+    // tid / 64, block tid / 32 % 2, feature tid % 32); pair blocks past dout
+    // read the zero sink.
+    auto bias_entry = [&](const Tile& Tb) KVX_INLINE -> float {
+      const int pb = Tb.nt * 4 + tid / 64;
+      const int npb = a.dout / 64, per_head = a.dt / 64;
+      const int f = (pb / per_head) * a.dt + 32 * (pb % per_head) + ((tid / 32) % 2) * (a.dt / 2) +
+                    tid % 32;
+      const float* q = pb < npb ? a.bias[Tb.kv] + static_cast<int64_t>(Tb.l) * a.dout + f
+                                : reinterpret_cast<const float*>(a.zsink);
+      return *q;
+    };
+    // tile 0's bias now; each later tile's is loaded during the previous
+    // tile's epilogue step and written at the end of its own first step
+    biasl[0][tid] = bias_entry(decode_tile(a, tbeg));
+    float bias_next = bias_entry(decode_tile(a, tbeg + 1 < tend ? tbeg + 1 : tbeg));
     auto end_step = [&]() KVX_INLINE {
+      if (s % spt == 0 && s > 0) biasl[(s / spt) % 2][tid] = bias_next;
       if (s % spt == nch) {
         lds_barrier();
         const int tau = tbeg + s / spt;
         store_rows<PAGED>(a, decode_tile(a, tau), lds + (s % 2) * 2 * kPlane, tid, blk);
         load_blocks<PAGED>(a, decode_tile(a, tau + 1 < tend ? tau + 1 : tau), tid, blk);
+        bias_next = bias_entry(decode_tile(a, tau + 1 < tend ? tau + 1 : tau));
       }
       lds_barrier();
       ++s;
@@ -608,31 +638,26 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   // Bias, target RoPE on K, bf16, into the staging buffer [token][256 + 8]:
   // lane holds, for token column lane%32 of token block m, the features
   // 8*(v/4) + 4*(lane/32) + v%4 (v < 16) of blocks c0 and c1; staged at
-  // column cw*64 + p*32 + feature offset.  Bias and frequencies come from
-  // wave-uniform scalar loads (read-only data).
-  auto stage = [&](const Tile& Tc, const Blocks& B, bf16_t* st) KVX_INLINE {
-    typedef const __attribute__((address_space(4))) float* cfloat_p;
-    typedef const __attribute__((address_space(4))) double* cdouble_p;
-    const int l_u = __builtin_amdgcn_readfirstlane(Tc.l);
-    const int kv_u = __builtin_amdgcn_readfirstlane(Tc.kv);
-    const int c0u = __builtin_amdgcn_readfirstlane(B.c0);
-    const int c1u = __builtin_amdgcn_readfirstlane(B.c1);
-    const int qu = __builtin_amdgcn_readfirstlane(B.q);
-    const cfloat_p bl = (cfloat_p)(a.bias[kv_u] + static_cast<int64_t>(l_u) * a.dout);
-    const cdouble_p fr = (cdouble_p)(a.ft);
-    const bool upper = lane >= 32;
+  // column cw*64 + p*32 + feature offset.  Bias comes from the tile's LDS
+  // copy; the RoPE angle is formed in fp64 for token block 0 and advanced by
+  // 32 positions per block with the rotation by 32 positions.
+  auto stage = [&](const Tile& Tc, const Blocks& B, bf16_t* st, const float* bias_t) KVX_INLINE {
+    const bool is_k = Tc.kv == 0;
+    const float* bl = bias_t + cw * 64 + fq;
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
-      float b0[8], b1[8];
+      const f32x4 b0 = *reinterpret_cast<const f32x4*>(bl + 8 * g4);
+      const f32x4 b1 = *reinterpret_cast<const f32x4*>(bl + 32 + 8 * g4);
+      float cs[4], sn[4], c32[4], s32[4];
+      if (is_k) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        b0[k] = bl[c0u + 8 * g4 + k];
-        b1[k] = bl[c1u + 8 * g4 + k];
-      }
-      double f8[8];
-      if (kv_u == 0) {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) f8[k] = fr[32 * qu + 8 * g4 + k];
+        for (int i = 0; i < 4; ++i) {
+          const int fi = 32 * B.q + 8 * g4 + fq + i;
+          rope_cs(ftl[fi], Tc.t0 + lane % 32, cs[i], sn[i]);
+          const float2 r = rot32[fi];
+          c32[i] = r.x;
+          s32[i] = r.y;
+        }
       }
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
@@ -640,18 +665,20 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         float u0[4], u1[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          u0[i] = acc[m][0][4 * g4 + i] + (upper ? b0[4 + i] : b0[i]);
-          u1[i] = acc[m][1][4 * g4 + i] + (upper ? b1[4 + i] : b1[i]);
+          u0[i] = acc[m][0][4 * g4 + i] + b0[i];
+          u1[i] = acc[m][1][4 * g4 + i] + b1[i];
         }
-        if (kv_u == 0) {
+        if (is_k) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            float cs, sn;
-            rope_cs(upper ? f8[4 + i] : f8[i], Tc.t0 + row, cs, sn);
-            const float y0 = u0[i] * cs - u1[i] * sn;
-            const float y1 = u1[i] * cs + u0[i] * sn;
+            const float y0 = u0[i] * cs[i] - u1[i] * sn[i];
+            const float y1 = u1[i] * cs[i] + u0[i] * sn[i];
             u0[i] = y0;
             u1[i] = y1;
+            // angle of token block m + 1
+            const float c2 = cs[i] * c32[i] - sn[i] * s32[i];
+            sn[i] = sn[i] * c32[i] + cs[i] * s32[i];
+            cs[i] = c2;
           }
         }
         const bf16x2 p00 = {static_cast<__bf16>(u0[0]), static_cast<__bf16>(u0[1])};
@@ -770,7 +797,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       lds_barrier();
     } else {
       // ---------------- epilogue step ----------------
-      if (B.on) stage(T, B, buf);
+      if (B.on) stage(T, B, buf, biasl[(s / spt) % 2]);
       lds_barrier();  // staging complete; the producers store the rows
       lds_barrier();
       if (cs < nchunks) {
