@@ -246,13 +246,23 @@ __device__ __forceinline__ void load_blocks(const FusedArgs& a, const Tile& Tc, 
   }
 }
 
-// Whole 16-byte pieces of target rows from the staging buffer [token][kNT+8]
-// of tile Tc (staged column w*64 + p*32 + j holds feature c_p + j of pair
-// block 4*nt + w); thread `it` of 256.
+// Staging layout of a finished tile.  Producer thread `it` stores the
+// 16-byte pieces (row it / 32 + 8 j, staged column 8 * (it % 32)), j < 16;
+// piece j lives in the A-buffer slot that the same thread fills in its
+// transform (plane j / 8, unit (j % 8) / 2, half j % 2).  A producer
+// therefore reads all of its staged pieces before its next transform
+// overwrites them, without any other thread touching them in between, and
+// the stores can run in the step after the staging.  Staged column
+// w*64 + p*32 + e holds feature c_p + e of pair block 4*nt + w.
+__device__ __forceinline__ int stage_slot(int it, int j) {
+  return (j / 8) * kPlane + (it / 8 + 32 * ((j % 8) / 2)) * kLDA + 64 * (j % 2) + 8 * (it % 8);
+}
+
+// Whole 16-byte pieces of target rows from the staged tile Tc; thread `it`
+// of 256.
 template <bool PAGED>
 __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, const bf16_t* st,
                                            int it, const int32_t (&blk)[kRowsPerThread]) {
-  constexpr int LDO = kNT + 8;
   const int npb = a.dout / 64;
   const int per_head = a.dt / 64;
   bf16_t* dst = a.tgt[Tc.kv] + Tc.l * a.ts.l;
@@ -276,7 +286,7 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
                               : static_cast<int64_t>(Tc.b) * a.ts.b + static_cast<int64_t>(t) * a.ts.t;
     bf16_t* q = dst + hd * a.ts.h + row + d;
     q = (t < Tc.tt && pbw < npb) ? q : a.trash;
-    st_stream(q, *reinterpret_cast<const uint4*>(st + r * LDO + sc8 * 8));
+    st_stream(q, *reinterpret_cast<const uint4*>(st + stage_slot(it, i)));
   }
 }
 
@@ -289,10 +299,12 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
 // step; every step ends with a workgroup barrier and step s owns LDS buffer
 // s % 2.  In a chunk step the consumers contract the buffer the producers
 // filled during the previous step.  In the epilogue step the consumers stage
-// the finished tile in their buffer (a mid-step barrier separates staging
-// from the row stores), while the producers fill the other buffer with the
-// next tile's first chunk.  Producers prefetch raw source data two chunks
-// ahead into registers.
+// the finished tile in their buffer while the producers fill the other
+// buffer with the next tile's first chunk; the producers write the staged
+// rows either after a mid-step barrier or at the start of the following
+// step, each from its own slots, before its transform reuses them.
+// Producers prefetch raw source data two or three chunks ahead into
+// registers.
 //
 // PREC: how computed operands (de-rotated K, pooled V) reach the matrix
 // cores -- split into two bf16 terms (kBF16X2), rounded once to bf16 (kBF16)
@@ -305,6 +317,10 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
 // re-reads them).  PAGED: target rows go through the block table.
 template <bool IDENT, bool CS_CACHE, int PREC, bool STREAM, bool PAGED>
 __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
+  // Row stores in the step after the staging (identity alignment), or in the
+  // epilogue step itself after a mid-step barrier (span maps: the pooling
+  // loop's dependent loads would otherwise wait behind the stores).
+  constexpr bool kDeferStores = IDENT;
   __shared__ __attribute__((aligned(16))) bf16_t lds[fused_lds_bytes() / 2];
   // layer map and source RoPE frequencies: per-lane lookups go to LDS, so no
   // vector load inside the step loop can queue behind outstanding stores
@@ -547,17 +563,26 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // tile's epilogue step and written at the end of its own first step
     biasl[0][tid] = bias_entry(decode_tile(a, tbeg));
     float bias_next = bias_entry(decode_tile(a, tbeg + 1 < tend ? tbeg + 1 : tbeg));
+    // Rows of tile tau staged in buffer sb, then the block ids of the next.
+    auto store_tile = [&](int tau, int sb) KVX_INLINE {
+      store_rows<PAGED>(a, decode_tile(a, tau), lds + sb * 2 * kPlane, tid, blk);
+      load_blocks<PAGED>(a, decode_tile(a, tau + 1 < tend ? tau + 1 : tau), tid, blk);
+    };
     auto end_step = [&]() KVX_INLINE {
       if (s % spt == 0 && s > 0) biasl[(s / spt) % 2][tid] = bias_next;
       if (s % spt == nch) {
-        lds_barrier();
         const int tau = tbeg + s / spt;
-        store_rows<PAGED>(a, decode_tile(a, tau), lds + (s % 2) * 2 * kPlane, tid, blk);
-        load_blocks<PAGED>(a, decode_tile(a, tau + 1 < tend ? tau + 1 : tau), tid, blk);
+        if (!kDeferStores) {
+          lds_barrier();  // staging complete
+          store_tile(tau, s % 2);
+        }
         bias_next = bias_entry(decode_tile(a, tau + 1 < tend ? tau + 1 : tau));
       }
       lds_barrier();
       ++s;
+      // deferred: the tile staged in step s - 1, before this thread's
+      // transform of step s reuses the slots
+      if (kDeferStores && s % spt == 0) store_tile(tbeg + s / spt - 1, (s - 1) % 2);
     };
     // Transform chunk `next` (consumed at step step_of(next)) during the step
     // before it, from raw set R, and refill R with chunk next + kDepth.
@@ -602,10 +627,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   const int trow = lane % 32;
   const int tcol = 8 * (lane / 32);
   const int fq = 4 * (lane / 32);
-  constexpr int LDO = kNT + 8;            // staging row stride (bf16)
 
   struct Blocks {
-    bool on;
+    int on;
     int c0, c1, q, hp;
     const bf16x8* w0p;
     const bf16x8* w1p;
@@ -626,16 +650,17 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   };
 
   f32x16 acc[4][2];
-  bf16x8 wf[8][2];
+  // weight fragments of k-steps ks .. ks + 3 (ring of four)
+  bf16x8 wf[4][2];
   auto load_w = [&](const Blocks& B, int c) KVX_INLINE {
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
+    for (int ks = 0; ks < 4; ++ks) {
       wf[ks][0] = B.w0p[(c * 8 + ks) * 64];
       wf[ks][1] = B.w1p[(c * 8 + ks) * 64];
     }
   };
 
-  // Bias, target RoPE on K, bf16, into the staging buffer [token][256 + 8]:
+  // Bias, target RoPE on K, bf16, into the staging slots (stage_slot):
   // lane holds, for token column lane%32 of token block m, the features
   // 8*(v/4) + 4*(lane/32) + v%4 (v < 16) of blocks c0 and c1; staged at
   // column cw*64 + p*32 + feature offset.  Bias comes from the tile's LDS
@@ -685,7 +710,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         const bf16x2 p01 = {static_cast<__bf16>(u0[2]), static_cast<__bf16>(u0[3])};
         const bf16x2 p10 = {static_cast<__bf16>(u1[0]), static_cast<__bf16>(u1[1])};
         const bf16x2 p11 = {static_cast<__bf16>(u1[2]), static_cast<__bf16>(u1[3])};
-        bf16_t* sp = st + row * LDO + cw * 64 + 8 * g4 + fq;
+        // staged columns cw*64 + p*32 + 8*g4 + fq .. +3 of this row (p = 1:
+        // piece owner it + 4, whose slot is 32 elements further)
+        bf16_t* sp = st + stage_slot((row % 8) * 32 + cw * 8 + g4, row / 8) + fq;
         *reinterpret_cast<uint2*>(sp) =
             make_uint2(__builtin_bit_cast(uint32_t, p00), __builtin_bit_cast(uint32_t, p01));
         *reinterpret_cast<uint2*>(sp + 32) =
@@ -696,6 +723,8 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
 
   Tile T = decode_tile(a, tbeg);
   Blocks B = blocks(T, cw);
+  Tile Tn = T;      // next tile (decoded in the step that loads its weights)
+  Blocks Bn = B;
   load_w(B, 0);  // valid addresses even for a pair block past dout
   lds_barrier();
   int cs = 0;  // global chunk index
@@ -704,91 +733,77 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     if (s % spt < nch) {
       // ---------------- chunk step ----------------
       const int c = s % spt;
-      if (c == 0) {
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-#pragma unroll
-          for (int p = 0; p < 2; ++p)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[m][p][v] = 0.f;
-      }
       const bool computed = T.kv == 0 || !IDENT;
-      // weights of the next chunk (possibly of the next tile): fragment ks is
-      // reloaded as soon as the MFMAs of k-step ks have issued, so each load
-      // has about one step to arrive
-      Blocks Bn = B;
+      // weights four k-steps ahead (k-steps 4..7 of this chunk, then 0..3 of
+      // the next chunk, possibly of the next tile): a ring slot is reloaded
+      // as soon as the MFMAs of its k-step have issued
       int cn = 0;
       const bool more = cs + 1 < nchunks;
+      if (c == 0) Bn = B;
       if (more) {
         cn = (cs + 1) % nch;
-        if (cn == 0) Bn = blocks(decode_tile(a, tbeg + (cs + 1) / nch), cw);
+        if (cn == 0) {
+          Tn = decode_tile(a, tbeg + (cs + 1) / nch);
+          Bn = blocks(Tn, cw);
+        }
       }
       // unconditional (past the last chunk, or for a pair block past dout, the
       // addresses are still valid fragments): the compiler then counts the
       // outstanding loads exactly instead of draining them all
       auto reload = [&](int ks) KVX_INLINE {
-        wf[ks][0] = Bn.w0p[(cn * 8 + ks) * 64];
-        wf[ks][1] = Bn.w1p[(cn * 8 + ks) * 64];
+        if (ks < 4) {
+          wf[ks][0] = B.w0p[(c * 8 + ks + 4) * 64];
+          wf[ks][1] = B.w1p[(c * 8 + ks + 4) * 64];
+        } else {
+          wf[ks - 4][0] = Bn.w0p[(cn * 8 + ks - 4) * 64];
+          wf[ks - 4][1] = Bn.w1p[(cn * 8 + ks - 4) * 64];
+        }
       };
       if (B.on) {
         const bf16_t* hi = buf;
         const bf16_t* lo = buf + kPlane;
-        if (PREC == kF16) {
-          // token fragments of k-step ks+1 are read while the MFMAs of ks run
-          f16x8 zc[4], zn[4];
+        // MFMA groups run in the order (k-step, plane): the token fragments of
+        // group g + 1 are read before the MFMAs of group g issue, so the LDS
+        // latency hides behind eight MFMAs; the scheduling barriers keep the
+        // compiler from sinking the reads next to their first use.
+        auto frag = [&](const bf16_t* plane, int ks, bf16x8 (&z)[4]) KVX_INLINE {
 #pragma unroll
           for (int m = 0; m < 4; ++m)
-            zc[m] = *reinterpret_cast<const f16x8*>(hi + (m * 32 + trow) * kLDA + tcol);
+            z[m] = *reinterpret_cast<const bf16x8*>(plane + (m * 32 + trow) * kLDA + ks * 16 + tcol);
+        };
+        // `fresh`: the tile's first MFMAs, which start from zero accumulators
+        // (an inline-constant source, so no register clearing)
+        auto mfma8 = [&](int ks, const bf16x8 (&z)[4], bool fresh) KVX_INLINE {
+          const f32x16 zero = {};
 #pragma unroll
-          for (int ks = 0; ks < 8; ++ks) {
-            if (ks + 1 < 8) {
+          for (int m = 0; m < 4; ++m) {
 #pragma unroll
-              for (int m = 0; m < 4; ++m)
-                zn[m] = *reinterpret_cast<const f16x8*>(hi + (m * 32 + trow) * kLDA +
-                                                        (ks + 1) * 16 + tcol);
+            for (int p = 0; p < 2; ++p) {
+              const f32x16 cin = fresh ? zero : acc[m][p];
+              if (PREC == kF16)
+                acc[m][p] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+                    __builtin_bit_cast(f16x8, wf[ks % 4][p]), __builtin_bit_cast(f16x8, z[m]), cin,
+                    0, 0, 0);
+              else
+                acc[m][p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks % 4][p], z[m], cin, 0, 0, 0);
             }
-            const f16x8 w0 = __builtin_bit_cast(f16x8, wf[ks][0]);
-            const f16x8 w1 = __builtin_bit_cast(f16x8, wf[ks][1]);
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-              acc[m][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w0, zc[m], acc[m][0], 0, 0, 0);
-              acc[m][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(w1, zc[m], acc[m][1], 0, 0, 0);
-            }
-            reload(ks);
-#pragma unroll
-            for (int m = 0; m < 4; ++m) zc[m] = zn[m];
           }
-        } else {
-          const bool split = PREC == kBF16X2 && computed;
+        };
+        const bool split = PREC == kBF16X2 && computed;
+        bf16x8 za[4], zb[4];
+        frag(hi, 0, za);
 #pragma unroll
-          for (int ks = 0; ks < 8; ++ks) {
-            bf16x8 zh[4];
-#pragma unroll
-            for (int m = 0; m < 4; ++m)
-              zh[m] =
-                  *reinterpret_cast<const bf16x8*>(hi + (m * 32 + trow) * kLDA + ks * 16 + tcol);
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-              acc[m][0] =
-                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][0], zh[m], acc[m][0], 0, 0, 0);
-              acc[m][1] =
-                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][1], zh[m], acc[m][1], 0, 0, 0);
-            }
-            if (split) {
-#pragma unroll
-              for (int m = 0; m < 4; ++m)
-                zh[m] = *reinterpret_cast<const bf16x8*>(lo + (m * 32 + trow) * kLDA + ks * 16 +
-                                                         tcol);
-#pragma unroll
-              for (int m = 0; m < 4; ++m) {
-                acc[m][0] =
-                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][0], zh[m], acc[m][0], 0, 0, 0);
-                acc[m][1] =
-                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[ks][1], zh[m], acc[m][1], 0, 0, 0);
-              }
-            }
-            reload(ks);
-          }
+        for (int ks = 0; ks < 8; ++ks) {
+          if (split) frag(lo, ks, zb);
+          __builtin_amdgcn_sched_barrier(0);
+          if (ks == 0 && c == 0) mfma8(ks, za, true);
+          else mfma8(ks, za, false);
+          __builtin_amdgcn_sched_barrier(0);
+          if (ks + 1 < 8) frag(hi, ks + 1, za);
+          __builtin_amdgcn_sched_barrier(0);
+          if (split) mfma8(ks, zb, false);
+          reload(ks);
+          __builtin_amdgcn_sched_barrier(0);
         }
       } else {
         load_w(Bn, cn);
@@ -798,11 +813,11 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     } else {
       // ---------------- epilogue step ----------------
       if (B.on) stage(T, B, buf, biasl[(s / spt) % 2]);
-      lds_barrier();  // staging complete; the producers store the rows
-      lds_barrier();
+      lds_barrier();  // staging complete
+      if (!kDeferStores) lds_barrier();  // the producers' row stores
       if (cs < nchunks) {
-        T = decode_tile(a, tbeg + cs / nch);
-        B = blocks(T, cw);
+        T = Tn;
+        B = Bn;
       }
     }
   }
