@@ -44,11 +44,13 @@ def _check(r, what):
 
 
 def build(out: str = LIB, verbose: bool = False) -> str:
-    """Compile the host library and the fused kernel's three precision
-    variants as separate objects (in parallel), then link libkvx.so."""
+    """Compile the host library, the translator fit and the fused kernel's
+    three precision variants as separate objects (in parallel), then link
+    libkvx.so."""
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
-    units = [("kvx", os.path.join(CSRC, "kvx.hip"), [])]
+    units = [("kvx", os.path.join(CSRC, "kvx.hip"), []),
+             ("fit", os.path.join(CSRC, "fit.hip"), [])]
     for i, name in enumerate(("bf16x2", "bf16", "f16")):
         units.append((f"fused_{name}", os.path.join(CSRC, "fused_launch.hip"),
                       [f"-DKVX_LAUNCH_PREC={i}"]))

@@ -1,0 +1,766 @@
+// fit.hip -- translator fit (kvx_fit.h): ridge least squares of the affine
+// per-layer translator from paired caches (the Section 5 objective with the
+// squared Frobenius distance).
+//
+// Device pipeline per batch of paired caches and group of target layers:
+//   fit_prepare  Z (pooled, source-de-rotated rows, plus a ones column for the
+//                bias) and Y (target rows de-rotated by the target RoPE) as
+//                feature-major bf16 planes hi/lo, X^T[plane][feature][row];
+//   fit_gram     acc[i][j] += sum_r X[r][i] X[r][j] for i over the Z features
+//                and j >= i over Z and Y (upper Z^T Z blocks and Z^T Y),
+//                v_mfma_f32_32x32x16_bf16 with hi*hi + hi*lo + lo*hi;
+// and once per solve:
+//   fit_solve    per system: A = Z^T Z + lam D (fp64), blocked Cholesky,
+//                forward and backward substitution for the Z^T Y columns,
+//                W = X^T[:din], b = X^T[din].
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "common.h"
+#include "kvx_fit.h"
+
+using namespace kvx;
+
+namespace {
+
+constexpr int kFB = 128;       // Gram block edge (features)
+constexpr int kSlab = 32;      // rows per LDS slab of the Gram kernel
+constexpr int kPitch = kSlab + 8;  // LDS pitch (bf16) of one feature's slab row
+constexpr int kFitBatch = 64;  // contexts per launch
+constexpr int kNB = 32;        // Cholesky panel width
+
+int32_t g_fit_hip = 0;
+
+kvx_status fit_hip_fail(hipError_t e) {
+  g_fit_hip = static_cast<int32_t>(e);
+  return e == hipErrorOutOfMemory ? KVX_ENOMEM : KVX_EHIP;
+}
+
+#define FIT_HIP(x)                                \
+  do {                                            \
+    hipError_t e_ = (x);                          \
+    if (e_ != hipSuccess) return fit_hip_fail(e_); \
+  } while (0)
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// Contexts of one launch: rows are concatenated per context.
+struct FitCtx {
+  int32_t n;
+  int32_t row0[kFitBatch + 1];  // first row (within the launch) of each context
+  int32_t csr0[kFitBatch];      // first CSR row of each context
+};
+
+struct PrepArgs {
+  const void* src[2];
+  Strides ss;
+  const void* tgt[2];
+  Strides ts;
+  const int32_t* row_ptr;  // nullptr: identity alignment
+  const int32_t* col_idx;
+  const float* weight;
+  const int32_t* layer_map;
+  const double* fs;  // source theta / 2pi (zeros without RoPE)
+  const double* ft;  // target theta / 2pi
+  int32_t mix, hs, ds, ht, dt;
+  int32_t din, dout, din_p, dout_p, F, rp, nrows, l0, fit_bias;
+  int32_t src_rope, tgt_rope;
+  bf16_t* xt;  // [sys][2][F][rp], sys = (l - l0) * 2 + kv
+  FitCtx ctx;
+};
+
+__device__ __forceinline__ int ctx_of(const FitCtx& c, int r) {
+  int lo = 0, hi = c.n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) / 2;
+    if (c.row0[mid] <= r) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ void split_store(bf16_t* hi, bf16_t* lo, const float (&v)[8]) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16_t h0 = f32_to_bf16(v[2 * i]), h1 = f32_to_bf16(v[2 * i + 1]);
+    const bf16_t l0 = f32_to_bf16(v[2 * i] - bf16_to_f32(h0));
+    const bf16_t l1 = f32_to_bf16(v[2 * i + 1] - bf16_to_f32(h1));
+    h[i] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+    l[i] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
+  }
+  *reinterpret_cast<uint4*>(hi) = make_uint4(h[0], h[1], h[2], h[3]);
+  *reinterpret_cast<uint4*>(lo) = make_uint4(l[0], l[1], l[2], l[3]);
+}
+
+// One thread: one job (a RoPE pair of Z, a pair of Y, or one padding / ones
+// feature) over 8 consecutive rows.  grid: x = job blocks, y = row groups of
+// 8 (grid-stride), z = systems of the layer group.
+template <typename T>
+__device__ __forceinline__ void prepare_rows(const PrepArgs& a, int job, int r0, int sys);
+
+template <typename T>
+__global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
+  const int job = blockIdx.x * 256 + threadIdx.x;
+  const int nz = a.din / 2, ny = a.dout / 2;
+  const int npad = (a.din_p - a.din) + (a.dout_p - a.dout);
+  if (job >= nz + ny + npad) return;
+  for (int r0 = blockIdx.y * 8; r0 < a.rp; r0 += gridDim.y * 8)
+    prepare_rows<T>(a, job, r0, blockIdx.z);
+}
+
+template <typename T>
+__device__ __forceinline__ void prepare_rows(const PrepArgs& a, int job, int r0, int sys) {
+  const int nz = a.din / 2, ny = a.dout / 2;
+  const int l = a.l0 + sys / 2;
+  const int kv = sys % 2;
+  bf16_t* base = a.xt + static_cast<int64_t>(sys) * 2 * a.F * a.rp;
+  bf16_t* lo_base = base + static_cast<int64_t>(a.F) * a.rp;
+  float v1[8], v2[8];
+  int f1, f2 = -1;
+  if (job < nz) {
+    // Z pair: mixed layer j, source head h, frequency i
+    const int half = a.ds / 2;
+    const int jh = job / half, i = job % half;
+    const int j = jh / a.hs, h = jh % a.hs;
+    const int ls = a.layer_map[l * a.mix + j];
+    f1 = jh * a.ds + i;
+    f2 = f1 + half;
+    const T* src = static_cast<const T*>(a.src[kv]) + ls * a.ss.l + h * a.ss.h + i;
+    const bool rot = kv == 0 && a.src_rope;
+    const double fr = a.fs[i];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int r = r0 + q;
+      float z1 = 0.f, z2 = 0.f;
+      if (r < a.nrows) {
+        const int b = ctx_of(a.ctx, r);
+        const int t = r - a.ctx.row0[b];
+        const T* sb = src + b * a.ss.b;
+        int e0 = 0, e1 = 1;
+        if (a.row_ptr) {
+          e0 = a.row_ptr[a.ctx.csr0[b] + t];
+          e1 = a.row_ptr[a.ctx.csr0[b] + t + 1];
+        }
+        for (int e = e0; e < e1; ++e) {
+          const int k = a.row_ptr ? a.col_idx[e] : t;
+          const float w = a.row_ptr ? a.weight[e] : 1.f;
+          const float x1 = load_f32<T>(sb + k * a.ss.t);
+          const float x2 = load_f32<T>(sb + k * a.ss.t + half);
+          float y1 = x1, y2 = x2;
+          if (rot) {
+            float c, s;
+            rope_cs(fr, k, c, s);
+            y1 = x1 * c + x2 * s;
+            y2 = x2 * c - x1 * s;
+          }
+          z1 += w * y1;
+          z2 += w * y2;
+        }
+      }
+      v1[q] = z1;
+      v2[q] = z2;
+    }
+  } else if (job < nz + ny) {
+    // Y pair: target head h, frequency i
+    const int p = job - nz;
+    const int half = a.dt / 2;
+    const int h = p / half, i = p % half;
+    f1 = a.din_p + h * a.dt + i;
+    f2 = f1 + half;
+    const T* tg = static_cast<const T*>(a.tgt[kv]) + l * a.ts.l + h * a.ts.h + i;
+    const bool rot = kv == 0 && a.tgt_rope;
+    const double fr = a.ft[i];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int r = r0 + q;
+      float y1 = 0.f, y2 = 0.f;
+      if (r < a.nrows) {
+        const int b = ctx_of(a.ctx, r);
+        const int t = r - a.ctx.row0[b];
+        const T* rowp = tg + b * a.ts.b + t * a.ts.t;
+        const float x1 = load_f32<T>(rowp), x2 = load_f32<T>(rowp + half);
+        y1 = x1;
+        y2 = x2;
+        if (rot) {
+          float c, s;
+          rope_cs(fr, t, c, s);
+          y1 = x1 * c + x2 * s;
+          y2 = x2 * c - x1 * s;
+        }
+      }
+      v1[q] = y1;
+      v2[q] = y2;
+    }
+  } else {
+    // padding features; the first one after Z is the ones column of the bias
+    const int p = job - nz - ny;
+    const int zpad = a.din_p - a.din;
+    f1 = p < zpad ? a.din + p : a.din_p + a.dout + (p - zpad);
+    const bool ones = a.fit_bias && f1 == a.din;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v1[q] = (ones && r0 + q < a.nrows) ? 1.f : 0.f;
+  }
+  split_store(base + static_cast<int64_t>(f1) * a.rp + r0,
+              lo_base + static_cast<int64_t>(f1) * a.rp + r0, v1);
+  if (f2 >= 0)
+    split_store(base + static_cast<int64_t>(f2) * a.rp + r0,
+                lo_base + static_cast<int64_t>(f2) * a.rp + r0, v2);
+}
+
+struct GramArgs {
+  const bf16_t* xt;   // [sys][2][F][rp]
+  float* acc;         // [sys_total][din_p][F]; this group starts at sys0
+  int32_t F, rp, nbi, nbj, sys0;
+};
+
+// One workgroup: one 128 x 128 block (bi, bj >= bi) of one system, all rows.
+// Four waves in 2 x 2, each 64 x 64 (2 x 2 MFMA tiles).  Slabs of 32 rows of
+// both feature blocks (hi and lo planes) are staged through LDS, double
+// buffered; the next slab is loaded into registers during the MFMAs.
+__global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t sl[2][2][2][kFB * kPitch];  // [stage][A|B][plane]
+  int x = blockIdx.x;
+  int bi = 0;
+  while (x >= a.nbj - bi) {
+    x -= a.nbj - bi;
+    ++bi;
+  }
+  const int bj = bi + x;
+  const int sys = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int wi = w / 2, wj = w % 2;
+  const bf16_t* xs = a.xt + static_cast<int64_t>(sys) * 2 * a.F * a.rp;
+  const int64_t plane = static_cast<int64_t>(a.F) * a.rp;
+
+  // loader: piece p = tid + 256 * u (u < 2) of a 128-feature x 32-row slab
+  // plane: feature p / 4, 16-byte column p % 4; 2 blocks x 2 planes x 2.
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 ld[2][2][2];
+  auto load_slab = [&](int r0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int ab = 0; ab < 2; ++ab)
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int p = tid + 256 * u;
+          const int f = (ab ? bj : bi) * kFB + p / 4;
+          ld[ab][pl][u] = *reinterpret_cast<const u32x4*>(xs + pl * plane +
+                                                          static_cast<int64_t>(f) * a.rp + r0 +
+                                                          (p % 4) * 8);
+        }
+  };
+  auto store_slab = [&](int st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int ab = 0; ab < 2; ++ab)
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int p = tid + 256 * u;
+          *reinterpret_cast<u32x4*>(&sl[st][ab][pl][(p / 4) * kPitch + (p % 4) * 8]) =
+              ld[ab][pl][u];
+        }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int nslab = a.rp / kSlab;
+  load_slab(0);
+  store_slab(0);
+  __syncthreads();
+  for (int s = 0; s < nslab; ++s) {
+    const int st = s % 2;
+    if (s + 1 < nslab) load_slab((s + 1) * kSlab);
+#pragma unroll
+    for (int ks = 0; ks < kSlab / 16; ++ks) {
+      bf16x8 fa[2][2], fb[2][2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl) {
+          fa[t][pl] = *reinterpret_cast<const bf16x8*>(
+              &sl[st][0][pl][(wi * 64 + t * 32 + lane % 32) * kPitch + ks * 16 + 8 * (lane / 32)]);
+          fb[t][pl] = *reinterpret_cast<const bf16x8*>(
+              &sl[st][1][pl][(wj * 64 + t * 32 + lane % 32) * kPitch + ks * 16 + 8 * (lane / 32)]);
+        }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i][0], fb[j][0], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i][0], fb[j][1], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i][1], fb[j][0], acc[i][j], 0, 0, 0);
+        }
+    }
+    if (s + 1 < nslab) {
+      store_slab(st ^ 1);
+    }
+    __syncthreads();
+  }
+  // D register v of lane l: row 8*(v/4) + 4*(l/32) + v%4, column l%32
+  float* out = a.acc + static_cast<int64_t>(a.sys0 + sys) * (a.nbi * kFB) * a.F;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = bi * kFB + wi * 64 + i * 32 + 8 * (v / 4) + 4 * (lane / 32) + v % 4;
+        const int col = bj * kFB + wj * 64 + j * 32 + lane % 32;
+        float* q = out + static_cast<int64_t>(row) * a.F + col;
+        *q += acc[i][j][v];
+      }
+}
+
+struct SolveArgs {
+  const float* acc;  // [sys][din_p][F]
+  double* A;         // [sys][n][n] scratch
+  double* X;         // [sys][n][dout] scratch (right-hand sides, then solution)
+  float* w[2];       // [Lt][dout][din]
+  float* b[2];       // [Lt][dout] or nullptr
+  int32_t* status;   // set to 1 if a pivot is not positive
+  double lam;
+  int32_t n, din, dout, din_p, F, fit_bias;
+};
+
+// One workgroup per system (l, kv): blocked right-looking Cholesky of
+// A = Zt^T Zt + lam D in fp64, then L L^T X = Zt^T Y.
+__global__ void __launch_bounds__(256) fit_solve(SolveArgs a) {
+  __shared__ double pk[kNB][kNB + 1];   // diagonal block / factor
+  __shared__ double pr[kNB][kNB + 1];   // panel rows (tile i)
+  __shared__ double pc[kNB][kNB + 1];   // panel rows (tile j)
+  const int sys = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int n = a.n, m = a.dout;
+  const float* acc = a.acc + static_cast<int64_t>(sys) * a.din_p * a.F;
+  double* A = a.A + static_cast<int64_t>(sys) * n * n;
+  double* X = a.X + static_cast<int64_t>(sys) * n * m;
+
+  // lower triangle of A from the upper accumulator blocks; ridge on Z only
+  for (int64_t idx = tid; idx < static_cast<int64_t>(n) * n; idx += 256) {
+    const int i = static_cast<int>(idx / n), j = static_cast<int>(idx % n);
+    if (j > i) continue;
+    double v = acc[static_cast<int64_t>(j) * a.F + i];
+    if (i == j && i < a.din) v += a.lam;
+    A[static_cast<int64_t>(i) * n + j] = v;
+  }
+  for (int64_t idx = tid; idx < static_cast<int64_t>(n) * m; idx += 256) {
+    const int i = static_cast<int>(idx / m), c = static_cast<int>(idx % m);
+    X[idx] = acc[static_cast<int64_t>(i) * a.F + a.din_p + c];
+  }
+  __syncthreads();
+
+  bool bad = false;
+  for (int kb = 0; kb < n; kb += kNB) {
+    const int kw = min(kNB, n - kb);
+    // (1) factor the diagonal block in LDS
+    for (int idx = tid; idx < kNB * kNB; idx += 256) {
+      const int i = idx / kNB, j = idx % kNB;
+      pk[i][j] = (i < kw && j <= i) ? A[static_cast<int64_t>(kb + i) * n + kb + j] : 0.0;
+    }
+    __syncthreads();
+    for (int k = 0; k < kw; ++k) {
+      const double dkk = pk[k][k];
+      const bool ok = dkk > 0.0 && isfinite(dkk);
+      bad |= !ok;
+      const double d = ok ? sqrt(dkk) : 1.0;
+      __syncthreads();
+      if (tid == 0) pk[k][k] = d;
+      for (int i = k + 1 + tid; i < kw; i += 256) pk[i][k] /= d;
+      __syncthreads();
+      for (int idx = tid; idx < kNB * kNB; idx += 256) {
+        const int i = idx / kNB, j = idx % kNB;
+        if (i > k && j > k && j <= i && i < kw) pk[i][j] -= pk[i][k] * pk[j][k];
+      }
+      __syncthreads();
+    }
+    for (int idx = tid; idx < kNB * kNB; idx += 256) {
+      const int i = idx / kNB, j = idx % kNB;
+      if (i < kw && j <= i) A[static_cast<int64_t>(kb + i) * n + kb + j] = pk[i][j];
+    }
+    // (2) panel below: row i solves x L_kk^T = a_i (forward substitution)
+    for (int i = kb + kw + tid; i < n; i += 256) {
+      double* row = A + static_cast<int64_t>(i) * n + kb;
+      for (int q = 0; q < kw; ++q) {
+        double s = row[q];
+        for (int p = 0; p < q; ++p) s -= row[p] * pk[q][p];
+        row[q] = s / pk[q][q];
+      }
+    }
+    __syncthreads();
+    // (3) trailing update of the lower triangle, 32 x 32 tiles
+    const int t0 = kb + kw;
+    const int nt = (n - t0 + kNB - 1) / kNB;
+    for (int ti = 0; ti < nt; ++ti) {
+      for (int tj = 0; tj <= ti; ++tj) {
+        const int i0 = t0 + ti * kNB, j0 = t0 + tj * kNB;
+        for (int idx = tid; idx < kNB * kNB; idx += 256) {
+          const int r = idx / kNB, q = idx % kNB;
+          pr[r][q] = (i0 + r < n && q < kw) ? A[static_cast<int64_t>(i0 + r) * n + kb + q] : 0.0;
+          pc[r][q] = (j0 + r < n && q < kw) ? A[static_cast<int64_t>(j0 + r) * n + kb + q] : 0.0;
+        }
+        __syncthreads();
+        for (int idx = tid; idx < kNB * kNB; idx += 256) {
+          const int r = idx / kNB, c = idx % kNB;
+          const int i = i0 + r, j = j0 + c;
+          if (i < n && j < n && j <= i) {
+            double s = 0.0;
+            for (int q = 0; q < kw; ++q) s += pr[r][q] * pc[c][q];
+            A[static_cast<int64_t>(i) * n + j] -= s;
+          }
+        }
+        __syncthreads();
+      }
+    }
+  }
+  if (bad) a.status[0] = 1;
+  __syncthreads();
+
+  // forward: L Y = B (columns c in parallel)
+  for (int c = tid; c < m; c += 256) {
+    for (int i = 0; i < n; ++i) {
+      const double* li = A + static_cast<int64_t>(i) * n;
+      double s = X[static_cast<int64_t>(i) * m + c];
+      for (int p = 0; p < i; ++p) s -= li[p] * X[static_cast<int64_t>(p) * m + c];
+      X[static_cast<int64_t>(i) * m + c] = s / li[i];
+    }
+    // backward: L^T X = Y
+    for (int i = n - 1; i >= 0; --i) {
+      double s = X[static_cast<int64_t>(i) * m + c];
+      for (int p = i + 1; p < n; ++p)
+        s -= A[static_cast<int64_t>(p) * n + i] * X[static_cast<int64_t>(p) * m + c];
+      X[static_cast<int64_t>(i) * m + c] = s / A[static_cast<int64_t>(i) * n + i];
+    }
+  }
+  __syncthreads();
+  const int l = sys / 2, kv = sys % 2;
+  float* w = a.w[kv] + static_cast<int64_t>(l) * m * a.din;
+  for (int64_t idx = tid; idx < static_cast<int64_t>(m) * a.din; idx += 256) {
+    const int c = static_cast<int>(idx / a.din), i = static_cast<int>(idx % a.din);
+    w[idx] = static_cast<float>(X[static_cast<int64_t>(i) * m + c]);
+  }
+  if (a.b[kv])
+    for (int c = tid; c < m; c += 256)
+      a.b[kv][static_cast<int64_t>(l) * m + c] =
+          a.fit_bias ? static_cast<float>(X[static_cast<int64_t>(a.din) * m + c]) : 0.f;
+}
+
+bool valid_side(const kvx_model& m) {
+  return m.n_layers > 0 && m.n_kv_heads > 0 && m.head_dim > 0 && std::isfinite(m.rope_base);
+}
+
+std::vector<double> theta_table(const kvx_model& m) {
+  std::vector<double> f(m.head_dim / 2, 0.0);
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int i = 0; i < m.head_dim / 2; ++i) {
+    double th = 0.0;
+    if (m.inv_freq)
+      th = m.inv_freq[i];
+    else if (m.rope_base > 0.0)
+      th = std::pow(m.rope_base, -2.0 * i / m.head_dim);
+    f[i] = th / two_pi;
+  }
+  return f;
+}
+
+}  // namespace
+
+struct kvx_fit {
+  int device = 0;
+  kvx_model src{}, tgt{};
+  int32_t mix = 1, dtype = KVX_BF16, fit_bias = 1;
+  int32_t din = 0, dout = 0, din_p = 0, dout_p = 0, F = 0, n = 0;
+  int32_t src_rope = 0, tgt_rope = 0;
+  int32_t* layer_map = nullptr;
+  double* fs = nullptr;
+  double* ft = nullptr;
+  float* acc = nullptr;        // [Lt * 2][din_p][F]
+  void* scratch = nullptr;     // prepared operands
+  size_t scratch_bytes = 0;
+  void* solve_buf = nullptr;
+  size_t solve_bytes = 0;
+  int64_t rows = 0;
+};
+
+extern "C" {
+
+kvx_status kvx_fit_create(const kvx_fit_desc* d, kvx_fit** out) {
+  if (out) *out = nullptr;
+  if (!d || !out || !d->layer_map) return KVX_EINVAL;
+  if (!valid_side(d->src) || !valid_side(d->tgt) || d->mix < 1) return KVX_EINVAL;
+  if (d->dtype != KVX_F32 && d->dtype != KVX_BF16) return KVX_EINVAL;
+  if (d->fit_bias != 0 && d->fit_bias != 1) return KVX_EINVAL;
+  if (d->src.head_dim % 2 || d->tgt.head_dim % 2) return KVX_EUNSUPPORTED;
+  const int64_t lt = d->tgt.n_layers;
+  for (int64_t i = 0; i < lt * d->mix; ++i)
+    if (d->layer_map[i] < 0 || d->layer_map[i] >= d->src.n_layers) return KVX_EINVAL;
+  const int64_t din = int64_t(d->mix) * d->src.n_kv_heads * d->src.head_dim;
+  const int64_t dout = int64_t(d->tgt.n_kv_heads) * d->tgt.head_dim;
+  if (din > 16384 || dout > 16384) return KVX_ESHAPE;
+  for (const kvx_model* m : {&d->src, &d->tgt})
+    if (m->inv_freq)
+      for (int i = 0; i < m->head_dim / 2; ++i)
+        if (!std::isfinite(m->inv_freq[i])) return KVX_EINVAL;
+
+  kvx_fit* f = new (std::nothrow) kvx_fit();
+  if (!f) return KVX_ENOMEM;
+  auto fail = [&](kvx_status s) {
+    kvx_fit_destroy(f);
+    return s;
+  };
+  f->src = d->src;
+  f->tgt = d->tgt;
+  f->src.inv_freq = f->tgt.inv_freq = nullptr;
+  f->mix = d->mix;
+  f->dtype = d->dtype;
+  f->fit_bias = d->fit_bias;
+  f->din = static_cast<int32_t>(din);
+  f->dout = static_cast<int32_t>(dout);
+  f->n = f->din + f->fit_bias;
+  f->din_p = static_cast<int32_t>(round_up(f->n, kFB));
+  f->dout_p = static_cast<int32_t>(round_up(dout, kFB));
+  f->F = f->din_p + f->dout_p;
+  f->src_rope = (d->src.inv_freq || d->src.rope_base > 0) ? 1 : 0;
+  f->tgt_rope = (d->tgt.inv_freq || d->tgt.rope_base > 0) ? 1 : 0;
+  hipError_t e = hipGetDevice(&f->device);
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  const size_t mb = size_t(lt) * d->mix * sizeof(int32_t);
+  e = hipMalloc(&f->layer_map, mb);
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  e = hipMemcpy(f->layer_map, d->layer_map, mb, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  std::vector<double> fsv = theta_table(d->src), ftv = theta_table(d->tgt);
+  e = hipMalloc(&f->fs, fsv.size() * sizeof(double));
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  e = hipMalloc(&f->ft, ftv.size() * sizeof(double));
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  e = hipMemcpy(f->fs, fsv.data(), fsv.size() * sizeof(double), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  e = hipMemcpy(f->ft, ftv.data(), ftv.size() * sizeof(double), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  const size_t ab = size_t(lt) * 2 * f->din_p * f->F * sizeof(float);
+  e = hipMalloc(&f->acc, ab);
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  e = hipMemset(f->acc, 0, ab);
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  e = hipDeviceSynchronize();
+  if (e != hipSuccess) return fail(fit_hip_fail(e));
+  *out = f;
+  return KVX_OK;
+}
+
+kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream) {
+  if (!f || !io_in) return KVX_EINVAL;
+  kvx_fit_io io = *io_in;
+  if (io.batch < 0 || io.src_tokens < 0 || io.tgt_capacity < 0) return KVX_EINVAL;
+  if (io.batch == 0) return KVX_OK;
+  const bool identity = io.tgt_tokens == nullptr;
+  std::vector<int32_t> tt(io.batch);
+  int64_t rows = 0;
+  for (int b = 0; b < io.batch; ++b) {
+    const int32_t t = identity ? io.src_tokens : io.tgt_tokens[b];
+    if (t < 0) return KVX_EINVAL;
+    if (t > io.tgt_capacity) return KVX_ESHAPE;
+    tt[b] = t;
+    rows += t;
+  }
+  if (rows == 0) return KVX_OK;
+  if (!io.src_k || !io.src_v || !io.tgt_k || !io.tgt_v) return KVX_EINVAL;
+  if (!identity && (!io.row_ptr || !io.col_idx || !io.weight)) return KVX_EINVAL;
+  if (rows > INT32_MAX / 2) return KVX_ESHAPE;
+  const int64_t Hs = f->src.n_kv_heads, Ds = f->src.head_dim;
+  const int64_t Lt = f->tgt.n_layers, Ht = f->tgt.n_kv_heads, Dt = f->tgt.head_dim;
+  const int64_t B = io.batch;
+  auto all_zero = [](const int64_t* s) { return !s[0] && !s[1] && !s[2] && !s[3]; };
+  if (all_zero(io.src_stride)) {
+    io.src_stride[3] = Ds;
+    io.src_stride[2] = Ds * io.src_tokens;
+    io.src_stride[1] = Hs * io.src_stride[2];
+    io.src_stride[0] = B * io.src_stride[1];
+  }
+  if (all_zero(io.tgt_stride)) {
+    io.tgt_stride[3] = Dt;
+    io.tgt_stride[2] = Dt * int64_t(io.tgt_capacity);
+    io.tgt_stride[1] = Ht * io.tgt_stride[2];
+    io.tgt_stride[0] = B * io.tgt_stride[1];
+  }
+  for (int i = 0; i < 4; ++i)
+    if (io.src_stride[i] < 0 || io.tgt_stride[i] < 0) return KVX_ESHAPE;
+  if ((io.src_stride[3] < Ds && io.src_tokens > 1) ||
+      (io.tgt_stride[3] < Dt && io.tgt_capacity > 1))
+    return KVX_ESHAPE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int esz = f->dtype == KVX_F32 ? 4 : 2;
+
+  int64_t row_base = 0;
+  for (int64_t b0 = 0; b0 < B; b0 += kFitBatch) {
+    const int nb = static_cast<int>(std::min<int64_t>(kFitBatch, B - b0));
+    FitCtx ctx{};
+    ctx.n = nb;
+    int32_t r = 0;
+    for (int i = 0; i < nb; ++i) {
+      ctx.row0[i] = r;
+      ctx.csr0[i] = static_cast<int32_t>(row_base);
+      r += tt[b0 + i];
+      row_base += tt[b0 + i];
+    }
+    ctx.row0[nb] = r;
+    if (r == 0) continue;
+    const int32_t rp = static_cast<int32_t>(round_up(r, kSlab));
+    // layer groups sized so the prepared operands fit a 1 GiB scratch
+    const size_t per_layer = size_t(2) * 2 * f->F * rp * sizeof(bf16_t);
+    const int64_t lg = std::max<int64_t>(1, std::min<int64_t>(Lt, (size_t(1) << 30) / per_layer));
+    const size_t need = per_layer * lg;
+    if (need > f->scratch_bytes) {
+      if (f->scratch) {
+        FIT_HIP(hipStreamSynchronize(st));
+        FIT_HIP(hipFree(f->scratch));
+        f->scratch = nullptr;
+        f->scratch_bytes = 0;
+      }
+      FIT_HIP(hipMalloc(&f->scratch, need));
+      f->scratch_bytes = need;
+    }
+    const Strides ss{io.src_stride[0], io.src_stride[1], io.src_stride[2], io.src_stride[3]};
+    const Strides ts{io.tgt_stride[0], io.tgt_stride[1], io.tgt_stride[2], io.tgt_stride[3]};
+    for (int64_t l0 = 0; l0 < Lt; l0 += lg) {
+      const int nl = static_cast<int>(std::min<int64_t>(lg, Lt - l0));
+      PrepArgs pa{};
+      pa.src[0] = static_cast<const char*>(io.src_k) + b0 * io.src_stride[1] * esz;
+      pa.src[1] = static_cast<const char*>(io.src_v) + b0 * io.src_stride[1] * esz;
+      pa.ss = ss;
+      pa.tgt[0] = static_cast<const char*>(io.tgt_k) + b0 * io.tgt_stride[1] * esz;
+      pa.tgt[1] = static_cast<const char*>(io.tgt_v) + b0 * io.tgt_stride[1] * esz;
+      pa.ts = ts;
+      pa.row_ptr = identity ? nullptr : io.row_ptr;
+      pa.col_idx = io.col_idx;
+      pa.weight = io.weight;
+      pa.layer_map = f->layer_map;
+      pa.fs = f->fs;
+      pa.ft = f->ft;
+      pa.mix = f->mix;
+      pa.hs = static_cast<int32_t>(Hs);
+      pa.ds = static_cast<int32_t>(Ds);
+      pa.ht = static_cast<int32_t>(Ht);
+      pa.dt = static_cast<int32_t>(Dt);
+      pa.din = f->din;
+      pa.dout = f->dout;
+      pa.din_p = f->din_p;
+      pa.dout_p = f->dout_p;
+      pa.F = f->F;
+      pa.rp = rp;
+      pa.nrows = r;
+      pa.l0 = static_cast<int32_t>(l0);
+      pa.fit_bias = f->fit_bias;
+      pa.src_rope = f->src_rope;
+      pa.tgt_rope = f->tgt_rope;
+      pa.xt = static_cast<bf16_t*>(f->scratch);
+      pa.ctx = ctx;
+      const int jobs = f->din / 2 + f->dout / 2 + (f->din_p - f->din) + (f->dout_p - f->dout);
+      const dim3 pg((jobs + 255) / 256, std::min(rp / 8, 32768), nl * 2);
+      if (f->dtype == KVX_F32)
+        fit_prepare<float><<<pg, dim3(256), 0, st>>>(pa);
+      else
+        fit_prepare<bf16_t><<<pg, dim3(256), 0, st>>>(pa);
+      FIT_HIP(hipGetLastError());
+      GramArgs ga{};
+      ga.xt = static_cast<const bf16_t*>(f->scratch);
+      ga.acc = f->acc;
+      ga.F = f->F;
+      ga.rp = rp;
+      ga.nbi = f->din_p / kFB;
+      ga.nbj = f->F / kFB;
+      ga.sys0 = static_cast<int32_t>(l0 * 2);
+      int nblk = 0;
+      for (int bi = 0; bi < ga.nbi; ++bi) nblk += ga.nbj - bi;
+      fit_gram<<<dim3(nblk, nl * 2), dim3(256), 0, st>>>(ga);
+      FIT_HIP(hipGetLastError());
+    }
+  }
+  f->rows += rows;
+  return KVX_OK;
+}
+
+kvx_status kvx_fit_solve(kvx_fit* f, double lambda, float* w_k, float* w_v, float* b_k,
+                         float* b_v, void* stream) {
+  if (!f || !w_k || !w_v || !std::isfinite(lambda) || lambda < 0) return KVX_EINVAL;
+  if (f->fit_bias && (!b_k || !b_v)) return KVX_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t nsys = int64_t(f->tgt.n_layers) * 2;
+  const size_t abytes = size_t(nsys) * f->n * f->n * sizeof(double);
+  const size_t xbytes = size_t(nsys) * f->n * f->dout * sizeof(double);
+  const size_t need = abytes + xbytes + 256;
+  if (need > f->solve_bytes) {
+    if (f->solve_buf) {
+      FIT_HIP(hipStreamSynchronize(st));
+      FIT_HIP(hipFree(f->solve_buf));
+      f->solve_buf = nullptr;
+      f->solve_bytes = 0;
+    }
+    FIT_HIP(hipMalloc(&f->solve_buf, need));
+    f->solve_bytes = need;
+  }
+  char* base = static_cast<char*>(f->solve_buf);
+  int32_t* status = reinterpret_cast<int32_t*>(base + abytes + xbytes);
+  FIT_HIP(hipMemsetAsync(status, 0, sizeof(int32_t), st));
+  SolveArgs sa{};
+  sa.acc = f->acc;
+  sa.A = reinterpret_cast<double*>(base);
+  sa.X = reinterpret_cast<double*>(base + abytes);
+  sa.w[0] = w_k;
+  sa.w[1] = w_v;
+  sa.b[0] = b_k;
+  sa.b[1] = b_v;
+  sa.status = status;
+  sa.lam = lambda;
+  sa.n = f->n;
+  sa.din = f->din;
+  sa.dout = f->dout;
+  sa.din_p = f->din_p;
+  sa.F = f->F;
+  sa.fit_bias = f->fit_bias;
+  fit_solve<<<dim3(static_cast<unsigned>(nsys)), dim3(256), 0, st>>>(sa);
+  FIT_HIP(hipGetLastError());
+  int32_t h = 0;
+  FIT_HIP(hipMemcpyAsync(&h, status, sizeof h, hipMemcpyDeviceToHost, st));
+  FIT_HIP(hipStreamSynchronize(st));
+  return h ? KVX_EDATA : KVX_OK;
+}
+
+kvx_status kvx_fit_reset(kvx_fit* f, void* stream) {
+  if (!f) return KVX_EINVAL;
+  const size_t ab = size_t(f->tgt.n_layers) * 2 * f->din_p * f->F * sizeof(float);
+  FIT_HIP(hipMemsetAsync(f->acc, 0, ab, static_cast<hipStream_t>(stream)));
+  f->rows = 0;
+  return KVX_OK;
+}
+
+int64_t kvx_fit_rows(const kvx_fit* f) { return f ? f->rows : 0; }
+
+void kvx_fit_destroy(kvx_fit* f) {
+  if (!f) return;
+  if (f->layer_map) (void)hipFree(f->layer_map);
+  if (f->fs) (void)hipFree(f->fs);
+  if (f->ft) (void)hipFree(f->ft);
+  if (f->acc) (void)hipFree(f->acc);
+  if (f->scratch) (void)hipFree(f->scratch);
+  if (f->solve_buf) (void)hipFree(f->solve_buf);
+  delete f;
+}
+
+}  // extern "C"

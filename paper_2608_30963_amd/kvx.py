@@ -1,9 +1,12 @@
 """Python binding of ``libkvx.so`` (argument marshalling only).
 
-The three entry points carry the C names -- ``kvx_plan_create``,
-``kvx_translate``, ``kvx_plan_destroy`` -- and take torch tensors for device
+The entry points carry the C names -- ``kvx_plan_create``, ``kvx_translate``,
+``kvx_plan_destroy`` (include/kvx.h) and ``kvx_fit_create``,
+``kvx_fit_accumulate``, ``kvx_fit_solve``, ``kvx_fit_reset``,
+``kvx_fit_destroy`` (include/kvx_fit.h) -- and take torch tensors for device
 buffers (torch provides device memory and streams; it computes nothing here).
-Every step of the translation runs in the library's HIP kernels.
+Every step of the translation and of the fit runs in the library's HIP
+kernels.
 
 The library must have been built (``python -m paper_2608_30963_amd.build``);
 loading fails loudly otherwise -- there is no fallback path.
@@ -22,9 +25,10 @@ KVX_OK, KVX_EINVAL, KVX_ESHAPE, KVX_EUNSUPPORTED, KVX_ENOMEM, KVX_EHIP, KVX_EDAT
 KVX_F32, KVX_BF16 = 0, 1
 KVX_PREC_BF16X2, KVX_PREC_BF16, KVX_PREC_F16 = 0, 1, 2
 
-# Exported C symbols, as declared in include/kvx.h.
+# Exported C symbols, as declared in include/kvx.h and include/kvx_fit.h.
 SYMBOLS = ("kvx_plan_create", "kvx_translate", "kvx_plan_destroy", "kvx_status_string",
-           "kvx_last_hip_error", "kvx_plan_query")
+           "kvx_last_hip_error", "kvx_plan_query", "kvx_fit_create", "kvx_fit_accumulate",
+           "kvx_fit_solve", "kvx_fit_reset", "kvx_fit_rows", "kvx_fit_destroy")
 
 
 class KvxError(RuntimeError):
@@ -55,6 +59,20 @@ class IO(C.Structure):
                 ("block_size", C.c_int32), ("max_blocks", C.c_int32), ("num_blocks", C.c_int32)]
 
 
+class FitDesc(C.Structure):
+    _fields_ = [("src", Model), ("tgt", Model), ("mix", C.c_int32),
+                ("layer_map", C.c_void_p), ("dtype", C.c_int32), ("fit_bias", C.c_int32)]
+
+
+class FitIO(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("src_tokens", C.c_int32),
+                ("src_k", C.c_void_p), ("src_v", C.c_void_p), ("src_stride", C.c_int64 * 4),
+                ("tgt_tokens", C.c_void_p), ("row_ptr", C.c_void_p),
+                ("col_idx", C.c_void_p), ("weight", C.c_void_p),
+                ("tgt_k", C.c_void_p), ("tgt_v", C.c_void_p), ("tgt_stride", C.c_int64 * 4),
+                ("tgt_capacity", C.c_int32)]
+
+
 class PlanInfo(C.Structure):
     _fields_ = [("kernel", C.c_int32), ("tile_rows", C.c_int32), ("tile_cols", C.c_int32),
                 ("threads", C.c_int32), ("precision", C.c_int32), ("weight_bytes", C.c_int64)]
@@ -83,6 +101,19 @@ def load(path: str = LIB_PATH):
     lib.kvx_last_hip_error.restype = C.c_int32
     lib.kvx_plan_query.argtypes = [C.c_void_p, C.POINTER(PlanInfo)]
     lib.kvx_plan_query.restype = C.c_int
+    lib.kvx_fit_create.argtypes = [C.POINTER(FitDesc), C.POINTER(C.c_void_p)]
+    lib.kvx_fit_create.restype = C.c_int
+    lib.kvx_fit_accumulate.argtypes = [C.c_void_p, C.POINTER(FitIO), C.c_void_p]
+    lib.kvx_fit_accumulate.restype = C.c_int
+    lib.kvx_fit_solve.argtypes = [C.c_void_p, C.c_double, C.c_void_p, C.c_void_p, C.c_void_p,
+                                  C.c_void_p, C.c_void_p]
+    lib.kvx_fit_solve.restype = C.c_int
+    lib.kvx_fit_reset.argtypes = [C.c_void_p, C.c_void_p]
+    lib.kvx_fit_reset.restype = C.c_int
+    lib.kvx_fit_rows.argtypes = [C.c_void_p]
+    lib.kvx_fit_rows.restype = C.c_int64
+    lib.kvx_fit_destroy.argtypes = [C.c_void_p]
+    lib.kvx_fit_destroy.restype = None
     _lib = lib
     return lib
 
@@ -230,6 +261,132 @@ class Translator:
         if self.plan:
             kvx_plan_destroy(self.plan)
             self.plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---------------------------------------------------------------------------
+# Translator fit (include/kvx_fit.h)
+# ---------------------------------------------------------------------------
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def kvx_fit_create(src, tgt, mix: int, layer_map: Sequence[int], dtype: int,
+                   fit_bias: bool = True, src_inv_freq=None, tgt_inv_freq=None) -> int:
+    lib = load()
+    keep = []
+    lm = _host_array([int(x) for x in layer_map], C.c_int32)
+    keep.append(lm)
+    desc = FitDesc(_model(src, src_inv_freq, keep), _model(tgt, tgt_inv_freq, keep), int(mix),
+                   C.cast(lm, C.c_void_p).value, int(dtype), 1 if fit_bias else 0)
+    h = C.c_void_p()
+    st = lib.kvx_fit_create(C.byref(desc), C.byref(h))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_fit_create")
+    return h.value
+
+
+def make_fit_io(batch: int, src_tokens: int, src_k, src_v, tgt_k, tgt_v, tgt_capacity: int,
+                tgt_tokens=None, row_ptr=None, col_idx=None, weight=None,
+                src_stride=(0, 0, 0, 0), tgt_stride=(0, 0, 0, 0)):
+    keep = []
+    tt = None
+    if tgt_tokens is not None:
+        tt = _host_array([int(x) for x in tgt_tokens], C.c_int32)
+        keep.append(tt)
+    io = FitIO(int(batch), int(src_tokens), _ptr(src_k), _ptr(src_v),
+               (C.c_int64 * 4)(*[int(x) for x in src_stride]),
+               C.cast(tt, C.c_void_p).value if tt is not None else None,
+               _ptr(row_ptr), _ptr(col_idx), _ptr(weight), _ptr(tgt_k), _ptr(tgt_v),
+               (C.c_int64 * 4)(*[int(x) for x in tgt_stride]), int(tgt_capacity))
+    return io, keep
+
+
+def kvx_fit_accumulate(fit: int, io: FitIO, stream=None) -> int:
+    st = load().kvx_fit_accumulate(C.c_void_p(fit), C.byref(io), C.c_void_p(_stream_handle(stream)))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_fit_accumulate")
+    return st
+
+
+def kvx_fit_solve(fit: int, lam: float, w_k, w_v, b_k=None, b_v=None, stream=None) -> int:
+    st = load().kvx_fit_solve(C.c_void_p(fit), float(lam), _ptr(w_k), _ptr(w_v), _ptr(b_k),
+                              _ptr(b_v), C.c_void_p(_stream_handle(stream)))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_fit_solve")
+    return st
+
+
+def kvx_fit_reset(fit: int, stream=None) -> int:
+    st = load().kvx_fit_reset(C.c_void_p(fit), C.c_void_p(_stream_handle(stream)))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_fit_reset")
+    return st
+
+
+def kvx_fit_rows(fit: int) -> int:
+    return int(load().kvx_fit_rows(C.c_void_p(fit)))
+
+
+def kvx_fit_destroy(fit: Optional[int]) -> None:
+    load().kvx_fit_destroy(C.c_void_p(fit) if fit else None)
+
+
+class Fitter:
+    """RAII wrapper around a fit, for the tests and the benchmark."""
+
+    def __init__(self, src, tgt, mix, layer_map, dtype, fit_bias=True, src_inv_freq=None,
+                 tgt_inv_freq=None):
+        self.tgt, self.mix, self.src = tgt, mix, src
+        self.fit_bias = fit_bias
+        self.handle = kvx_fit_create(src, tgt, mix, layer_map, dtype, fit_bias, src_inv_freq,
+                                     tgt_inv_freq)
+
+    def accumulate(self, src_k, src_v, tgt_k, tgt_v, tgt_tokens=None, row_ptr=None,
+                   col_idx=None, weight=None, stream=None, src_stride=(0, 0, 0, 0),
+                   tgt_stride=(0, 0, 0, 0)):
+        """Source caches [Ls][B][Hs][T_s][Ds], native target caches
+        [Lt][B][Ht][cap][Dt] (torch device tensors)."""
+        batch, src_tokens = int(src_k.shape[1]), int(src_k.shape[3])
+        io, keep = make_fit_io(batch, src_tokens, src_k, src_v, tgt_k, tgt_v,
+                               int(tgt_k.shape[3]), tgt_tokens, row_ptr, col_idx, weight,
+                               src_stride, tgt_stride)
+        kvx_fit_accumulate(self.handle, io, stream)
+        del keep
+
+    def solve(self, lam, stream=None):
+        """Returns fp32 device tensors (w_k, w_v, b_k, b_v)."""
+        import torch
+        Lt = self.tgt.n_layers
+        dout = self.tgt.n_kv_heads * self.tgt.head_dim
+        din = self.mix * self.src.n_kv_heads * self.src.head_dim
+        w_k = torch.empty((Lt, dout, din), dtype=torch.float32, device="cuda")
+        w_v = torch.empty_like(w_k)
+        b_k = torch.empty((Lt, dout), dtype=torch.float32, device="cuda")
+        b_v = torch.empty_like(b_k)
+        kvx_fit_solve(self.handle, lam, w_k, w_v, b_k, b_v, stream)
+        return w_k, w_v, b_k, b_v
+
+    def reset(self, stream=None):
+        kvx_fit_reset(self.handle, stream)
+
+    @property
+    def rows(self) -> int:
+        return kvx_fit_rows(self.handle)
+
+    def close(self):
+        if self.handle:
+            kvx_fit_destroy(self.handle)
+            self.handle = None
 
     def __del__(self):
         try:

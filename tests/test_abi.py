@@ -9,13 +9,17 @@ import pytest
 
 from paper_2608_30963_amd import kvx
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
-                      "include", "kvx.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+HEADERS = [os.path.join(INCLUDE, h) for h in sorted(os.listdir(INCLUDE)) if h.endswith(".h")]
 
 
 def _declared():
-    text = open(HEADER).read()
-    return sorted(set(re.findall(r"\b(kvx_[a-z_]+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        # declarations: a line that starts with the return type
+        names |= set(re.findall(r"^(?:const\s+)?[a-z_0-9]+\**\s+\**(kvx_[a-z_]+)\s*\(",
+                                open(h).read(), flags=re.M))
+    return sorted(names)
 
 
 def test_every_declared_symbol_is_exported():
@@ -106,3 +110,45 @@ def test_translate_rejects_null_and_destroy_is_null_safe():
 def test_query_rejects_null():
     info = kvx.PlanInfo()
     assert kvx.load().kvx_plan_query(None, C.byref(info)) == kvx.KVX_EINVAL
+
+
+def _fit_desc(**kw):
+    src = kvx.Model(4, 2, 64, 1e4, None)
+    tgt = kvx.Model(4, 2, 64, 1e4, None)
+    lm = (C.c_int32 * 4)(0, 1, 2, 3)
+    base = dict(src=src, tgt=tgt, mix=1, layer_map=C.cast(lm, C.c_void_p).value,
+                dtype=kvx.KVX_BF16, fit_bias=1)
+    base.update(kw)
+    return kvx.FitDesc(**base), lm
+
+
+def _fit_create(desc):
+    h = C.c_void_p(12345)
+    st = kvx.load().kvx_fit_create(C.byref(desc), C.byref(h))
+    return st, h.value
+
+
+def test_fit_create_rejects_bad_arguments():
+    lib = kvx.load()
+    assert lib.kvx_fit_create(None, None) == kvx.KVX_EINVAL
+    for kw, status in (({"mix": 0}, kvx.KVX_EINVAL), ({"dtype": 5}, kvx.KVX_EINVAL),
+                       ({"fit_bias": 2}, kvx.KVX_EINVAL), ({"layer_map": None}, kvx.KVX_EINVAL),
+                       ({"src": kvx.Model(4, 2, 63, 1e4, None)}, kvx.KVX_EUNSUPPORTED),
+                       ({"tgt": kvx.Model(0, 2, 64, 1e4, None)}, kvx.KVX_EINVAL)):
+        d, keep = _fit_desc(**kw)
+        st, h = _fit_create(d)
+        assert st == status and h is None, kw
+    lm = (C.c_int32 * 4)(0, 1, 2, 9)
+    d, keep = _fit_desc(layer_map=C.cast(lm, C.c_void_p).value)
+    assert _fit_create(d)[0] == kvx.KVX_EINVAL
+
+
+def test_fit_calls_reject_null():
+    lib = kvx.load()
+    io, keep = kvx.make_fit_io(1, 4, 0x10, 0x10, 0x10, 0x10, 4)
+    assert lib.kvx_fit_accumulate(None, C.byref(io), None) == kvx.KVX_EINVAL
+    assert lib.kvx_fit_accumulate(C.c_void_p(1), None, None) == kvx.KVX_EINVAL
+    assert lib.kvx_fit_solve(None, 1.0, 0x10, 0x10, 0x10, 0x10, None) == kvx.KVX_EINVAL
+    assert lib.kvx_fit_reset(None, None) == kvx.KVX_EINVAL
+    assert lib.kvx_fit_rows(None) == 0
+    kvx.kvx_fit_destroy(None)

@@ -1,0 +1,213 @@
+"""GPU parity of the translator fit (include/kvx_fit.h) against the fp64 fit
+oracle (oracle/fit.py), which is pinned by tests/test_fit_oracle.py.
+
+Native target caches are made by the translation oracle from the problem's
+own weights, plus seeded Gaussian noise, and rounded to the storage dtype;
+both sides fit the same stored bits.
+
+Tolerances.  The device accumulates Zt^T [Zt Y] from operands split into two
+bf16 terms (relative product error about 2^-16) with fp32 sums, and solves in
+fp64.  A relative perturbation e of the normal equations moves the solution by
+about cond(A) * e, so W is compared in relative Frobenius norm against a bound
+of 1e-3 (moderately conditioned cases) or 2e-2 (x20 outlier channels); the
+least-squares objective, which is flat at the optimum, must match the
+oracle's optimum to 1e-5 relative.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from oracle import fit as F
+from oracle import oracle as O
+from paper_2608_30963_amd import kvx, synth as S
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+
+def _spec(**kw):
+    base = dict(cfg_id=400, name="fit", src=S.ModelShape(2, 2, 64, 1.0e4),
+                tgt=S.ModelShape(2, 2, 64, 1.0e6), mix=1, layer_map=(1, 0), dtype=S.BF16,
+                src_tokens=300, batch=2, bias_std=0.3, seed=1)
+    base.update(kw)
+    return S.Spec(**base)
+
+
+def _native(prob, noise, seed=11):
+    """Oracle-translated caches plus noise, rounded to the storage dtype."""
+    tk, tv = O.translate(prob)
+    rng = np.random.default_rng(seed)
+    out = []
+    for t in (tk, tv):
+        t = t + noise * rng.standard_normal(t.shape)
+        t = np.nan_to_num(t, nan=0.0).astype(np.float32)
+        out.append(S.to_storage(t, prob.spec.dtype))
+    return out
+
+
+def _gpu_fit(prob, tk, tv, lam, fit_bias=True, parts=None):
+    T = U.torch()
+    spec = prob.spec
+    dt = spec.dtype
+    fitter = kvx.Fitter(spec.src, spec.tgt, spec.mix, spec.layer_map,
+                        kvx.KVX_BF16 if dt == S.BF16 else kvx.KVX_F32, fit_bias)
+    dk, dv = U.np_to_dev(tk, dt), U.np_to_dev(tv, dt)
+    sk, sv = U.np_to_dev(prob.src_k, dt), U.np_to_dev(prob.src_v, dt)
+    ident = prob.row_ptr is None
+    if parts is None:
+        fitter.accumulate(sk, sv, dk, dv, None if ident else prob.tgt_tokens,
+                          None if ident else U.np_to_dev(prob.row_ptr, S.F32),
+                          None if ident else U.np_to_dev(prob.col_idx, S.F32),
+                          None if ident else U.np_to_dev(prob.weight, S.F32))
+    else:
+        assert ident
+        for b0, b1 in parts:       # contexts [b0, b1) as separate batches
+            fitter.accumulate(sk[:, b0:b1].contiguous(), sv[:, b0:b1].contiguous(),
+                              dk[:, b0:b1].contiguous(), dv[:, b0:b1].contiguous())
+    w_k, w_v, b_k, b_v = fitter.solve(lam)
+    T.cuda.synchronize()
+    rows = fitter.rows
+    fitter.close()
+    return [x.cpu().numpy().astype(np.float64) for x in (w_k, w_v, b_k, b_v)], rows
+
+
+def _compare(prob, tk, tv, got, lam, fit_bias, w_tol, what):
+    ref = F.fit(prob, tk, tv, lam, fit_bias)
+    for which, (gw, gb, rw, rb, tgt) in enumerate(((got[0], got[2], ref[0], ref[2], tk),
+                                                   (got[1], got[3], ref[1], ref[3], tv))):
+        name = f"{what} {'KV'[which]}"
+        assert np.isfinite(gw).all() and np.isfinite(gb).all(), name
+        rel = np.linalg.norm(gw - rw) / np.linalg.norm(rw)
+        assert rel <= w_tol, f"{name}: W relative error {rel:.3e} > {w_tol}"
+        if not fit_bias:
+            assert np.all(gb == 0.0), name
+        jo = F.objective(prob, tgt, which, gw, gb if fit_bias else None, lam)
+        jr = F.objective(prob, tgt, which, rw, rb if fit_bias else None, lam)
+        assert jo <= jr * (1 + 1e-5), f"{name}: objective {jo:.9e} vs optimum {jr:.9e}"
+        print(f"[fit] {name}: W rel err {rel:.2e}, objective excess {jo / jr - 1:.2e}",
+              flush=True)
+
+
+def test_fit_identity_bf16():
+    prob = S.make_problem(_spec())
+    tk, tv = _native(prob, noise=0.05)
+    print("[fit] identity bf16", flush=True)
+    got, rows = _gpu_fit(prob, tk, tv, lam=1.0)
+    assert rows == 600
+    _compare(prob, tk, tv, got, 1.0, True, 1e-3, "identity")
+
+
+def test_fit_spans_mix2_padded_output():
+    """Span alignment, two mixed source layers, dout = 64 (padded block)."""
+    spec = _spec(src=S.ModelShape(3, 2, 32, 1.0e4), tgt=S.ModelShape(2, 2, 32, 1.0e6), mix=2,
+                 layer_map=(0, 1, 2, 1), src_tokens=500, batch=1, span_lo=1, span_hi=3)
+    prob = S.make_problem(spec)
+    tk, tv = _native(prob, noise=0.05)
+    print("[fit] spans mix2", flush=True)
+    got, rows = _gpu_fit(prob, tk, tv, lam=0.5)
+    assert rows == int(prob.tgt_tokens.sum())
+    _compare(prob, tk, tv, got, 0.5, True, 1e-3, "spans")
+
+
+def test_fit_qwen_heads_outliers():
+    """Qwen2.5-7B -> 1.5B head geometry (din 512, dout 256) on two layers,
+    x20 outlier channels: the ones column pads Zt to 640 features."""
+    spec = _spec(src=S.ModelShape(2, 4, 128, 1.0e6), tgt=S.ModelShape(2, 2, 128, 1.0e6),
+                 src_tokens=700, batch=1, outliers=4)
+    prob = S.make_problem(spec)
+    tk, tv = _native(prob, noise=0.1)
+    print("[fit] qwen heads", flush=True)
+    got, _ = _gpu_fit(prob, tk, tv, lam=2.0)
+    _compare(prob, tk, tv, got, 2.0, True, 2e-2, "qwen")
+
+
+def test_fit_f32_without_bias():
+    spec = _spec(dtype=S.F32, bias_std=0.0, src_tokens=200)
+    prob = S.make_problem(spec)
+    tk, tv = _native(prob, noise=0.02)
+    print("[fit] f32 no bias", flush=True)
+    got, _ = _gpu_fit(prob, tk, tv, lam=0.1, fit_bias=False)
+    _compare(prob, tk, tv, got, 0.1, False, 1e-3, "f32")
+
+
+def test_fit_accumulates_across_calls():
+    """Three batches accumulated in turn give the one-batch fit."""
+    spec = _spec(batch=3, src_tokens=160)
+    prob = S.make_problem(spec)
+    tk, tv = _native(prob, noise=0.05)
+    print("[fit] parts", flush=True)
+    whole, rows_w = _gpu_fit(prob, tk, tv, lam=1.0)
+    parts, rows_p = _gpu_fit(prob, tk, tv, lam=1.0, parts=[(0, 1), (1, 3)])
+    assert rows_w == rows_p == 480
+    for a, b in zip(whole, parts):
+        assert np.linalg.norm(a - b) <= 1e-4 * max(np.linalg.norm(a), 1e-30)
+
+
+def test_fit_recovers_translator():
+    """Noise-free native caches (bf16-rounded): the fit returns the weights
+    that produced them, to the bf16 rounding of the targets."""
+    spec = _spec(src_tokens=400)
+    prob = S.make_problem(spec)
+    tk, tv = _native(prob, noise=0.0)
+    print("[fit] recovery", flush=True)
+    got, _ = _gpu_fit(prob, tk, tv, lam=1e-3)
+    for g, ref in ((got[0], prob.w_k), (got[1], prob.w_v)):
+        ref = F._widen(ref)
+        rel = np.linalg.norm(g - ref) / np.linalg.norm(ref)
+        assert rel <= 2e-2, rel
+    for g, ref in ((got[2], prob.b_k), (got[3], prob.b_v)):
+        assert np.max(np.abs(g - ref)) <= 5e-2
+
+
+def test_fit_errors_and_reset():
+    T = U.torch()
+    spec = _spec(src_tokens=64)
+    prob = S.make_problem(spec)
+    fitter = kvx.Fitter(spec.src, spec.tgt, spec.mix, spec.layer_map, kvx.KVX_BF16, True)
+    w = T.empty((2, 128, 128), dtype=T.float32, device="cuda")
+    b = T.empty((2, 128), dtype=T.float32, device="cuda")
+    with pytest.raises(kvx.KvxError) as e:
+        kvx.kvx_fit_solve(fitter.handle, -1.0, w, w, b, b)
+    assert e.value.status == kvx.KVX_EINVAL
+    # nothing accumulated: A = 0 has no positive pivot
+    with pytest.raises(kvx.KvxError) as e:
+        kvx.kvx_fit_solve(fitter.handle, 0.0, w, w, b, b)
+    assert e.value.status == kvx.KVX_EDATA
+    tk, tv = _native(prob, noise=0.05)
+    dk, dv = U.np_to_dev(tk, S.BF16), U.np_to_dev(tv, S.BF16)
+    sk, sv = U.np_to_dev(prob.src_k, S.BF16), U.np_to_dev(prob.src_v, S.BF16)
+    # capacity smaller than the context: rejected before any launch
+    io, keep = kvx.make_fit_io(2, 64, sk, sv, dk, dv, 32)
+    assert kvx.load().kvx_fit_accumulate(fitter.handle, io, None) == kvx.KVX_ESHAPE
+    fitter.accumulate(sk, sv, dk, dv)
+    assert fitter.rows == 128
+    fitter.reset()
+    assert fitter.rows == 0
+    with pytest.raises(kvx.KvxError) as e:
+        kvx.kvx_fit_solve(fitter.handle, 0.0, w, w, b, b)
+    assert e.value.status == kvx.KVX_EDATA
+    T.cuda.synchronize()
+    fitter.close()
+
+
+def test_fitted_weights_translate():
+    """End to end: weights fitted on the device, cast to bf16 and planned,
+    translate the source into caches close to the native ones."""
+    T = U.torch()
+    spec = _spec(src_tokens=256)
+    prob = S.make_problem(spec)
+    tk, tv = _native(prob, noise=0.0)
+    got, _ = _gpu_fit(prob, tk, tv, lam=1e-3)
+    fitted = dataclasses.replace(prob, w_k=S.to_storage(got[0].astype(np.float32), S.BF16),
+                                 w_v=S.to_storage(got[1].astype(np.float32), S.BF16),
+                                 b_k=got[2].astype(np.float32), b_v=got[3].astype(np.float32))
+    dev = U.DevProblem(fitted)
+    dev.run()
+    T.cuda.synchronize()
+    gk = U.dev_to_f64(dev.tgt_k, S.BF16)
+    nk = F._widen(tk)
+    rel = np.linalg.norm(gk - nk) / np.linalg.norm(nk)
+    print(f"[fit] end-to-end K relative distance {rel:.3e}", flush=True)
+    assert rel <= 3e-2
+    dev.close()
