@@ -13,6 +13,11 @@ synthetic data.  Inputs are resident in HBM before the timed region; three
 buffer sets rotate so no call finds its inputs in the 256 MB last-level cache.
 
 Prints one JSON line (rank 0).
+
+``--fit`` measures the translator fit instead (include/kvx_fit.h): a step is
+one ``kvx_fit_accumulate`` of the workload's paired caches (source cache and
+a seeded stand-in for the target model's own cache) into every layer's K and
+V normal equations; the solve is timed once afterwards.
 """
 from __future__ import annotations
 
@@ -136,6 +141,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--fit", action="store_true",
+                    help="measure the translator fit (accumulate + solve) instead")
+    ap.add_argument("--lam", type=float, default=1.0, help="ridge of the fit's solve")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="first run a plain device copy (bitwise_not) of this many MiB "
                          "(three times), "
@@ -161,6 +169,8 @@ def main():
     print(f"[bench] generating {spec.name} T={spec.src_tokens} B={spec.batch}",
           file=sys.stderr, flush=True)
     prob = S.make_problem(spec)
+    if args.fit:
+        return main_fit(args, spec, prob, torch, kvx, S)
     alg = algorithmic(spec, prob)
 
     def dev(a, f32=False):
@@ -312,6 +322,120 @@ def main():
     }
     print(json.dumps(out), flush=True)
     tr.close()
+
+
+def fit_flops(spec, rows: int, fit_bias: bool = True) -> int:
+    """Algorithmic flops of accumulating `rows` rows: per (layer, K|V) system
+    the symmetric Zt^T Zt (n(n+1)/2 entries) and Zt^T Y, 2 flops per term."""
+    n = spec.d_in + (1 if fit_bias else 0)
+    return 2 * spec.tgt.n_layers * 2 * rows * (n * (n + 1) // 2 + n * spec.d_out)
+
+
+def fit_cpu_baseline(spec, prob, tk, tv, lam: float, budget_s: float):
+    """The fp64 fit oracle on the host over as many target layers as fit the
+    budget (all rows, K and V), scaled to rows per second of the whole job."""
+    from oracle import fit as F
+    import dataclasses
+    rows = int(prob.tgt_tokens.sum())
+    done, t0 = 0, time.perf_counter()
+    for l in range(spec.tgt.n_layers):
+        sub = dataclasses.replace(spec, tgt=dataclasses.replace(spec.tgt, n_layers=1),
+                                  layer_map=tuple(spec.layer_map[l * spec.mix:(l + 1) * spec.mix]))
+        p1 = dataclasses.replace(prob, spec=sub, layer_map=np.asarray(sub.layer_map, np.int32))
+        F.fit(p1, tk[l:l + 1], tv[l:l + 1], lam, True)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": rows * done / spec.tgt.n_layers / el, "unit": "rows/s",
+            "cores": os.cpu_count(), "kind": "oracle",
+            "sample": f"fp64 numpy fit oracle, {done} of {spec.tgt.n_layers} target layers "
+                      f"(K and V, all {rows} rows), {el:.1f} s"}
+
+
+def main_fit(args, spec, prob, torch, kvx, S):
+    os.environ["KVX_FIT_TIMING"] = "1"
+    kd = kvx.KVX_BF16 if spec.dtype == "bf16" else kvx.KVX_F32
+    print("[bench] drawing native target caches", file=sys.stderr, flush=True)
+    tk = S.draw_native_target(spec, 0, prob.tgt_tokens)
+    tv = S.draw_native_target(spec, 1, prob.tgt_tokens)
+
+    def dev(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    sk, sv, dk, dv = dev(prob.src_k), dev(prob.src_v), dev(tk), dev(tv)
+    ident = prob.row_ptr is None
+    rp, ci, wt = (None, None, None) if ident else (dev(prob.row_ptr), dev(prob.col_idx),
+                                                  dev(prob.weight))
+    tt = None if ident else prob.tgt_tokens
+    fitter = kvx.Fitter(spec.src, spec.tgt, spec.mix, spec.layer_map, kd, True)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        fitter.accumulate(sk, sv, dk, dv, tt, rp, ci, wt, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    fitter.info()            # drop the warm-up launches' timing events
+    fitter.reset()
+    print(f"[bench] fit warmup done; timing {args.steps} accumulates", file=sys.stderr,
+          flush=True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    info = fitter.info()
+    ms_gram = info.gram_ms / max(1, info.gram_launches)
+    launches_per_step = info.gram_launches / args.steps
+    rows = int(prob.tgt_tokens.sum())
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record(stream)
+    w_k, w_v, b_k, b_v = fitter.solve(args.lam, stream=stream)
+    s1.record(stream)
+    torch.cuda.synchronize()
+    ms_solve = s0.elapsed_time(s1)
+    if not (torch.isfinite(w_k).all() and torch.isfinite(w_v).all()):
+        print("bench.py: fit produced non-finite weights", file=sys.stderr)
+        sys.exit(1)
+    flops_step = fit_flops(spec, rows)
+    flops_launch = flops_step / launches_per_step
+    tfs = flops_launch / (ms_gram * 1e-3) / 1e12
+    cpu = None
+    if not args.no_cpu and args.cpu_budget > 0:
+        print("[bench] timing the CPU fit oracle", file=sys.stderr, flush=True)
+        cpu = fit_cpu_baseline(spec, prob, tk, tv, args.lam, args.cpu_budget)
+    out = {
+        "metric": "fit rows/s (paired target tokens accumulated into every layer's K and V "
+                  "normal equations)",
+        "value": round(rows / (ms * 1e-3), 1), "unit": "rows/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16x2->fp32 accumulate, fp64 solve", "data": "synthetic",
+        "config": {"workload": f"translator fit, {spec.name}", "rows": rows,
+                   "src_tokens": spec.src_tokens, "batch": spec.batch,
+                   "systems": info.systems, "unknowns": info.n, "outputs": spec.d_out,
+                   "lambda": args.lam, "parallelism": "single GPU"},
+        "ms_per_solve": round(ms_solve, 3),
+        "roofline": {"bound": "mfma", "achieved": round(tfs, 1), "peak": MFMA_BF16_PEAK_TFS,
+                     "unit": "TFLOP/s", "frac": round(tfs / MFMA_BF16_PEAK_TFS, 4),
+                     "traffic": None, "kernel": "fit_gram",
+                     "flops_per_launch": int(flops_launch), "ms_per_launch": round(ms_gram, 5),
+                     "issued_mfma_flops_per_launch": int(
+                         3 * 2 * 128 * 128 * info.gram_blocks * info.systems * 32 *
+                         ((rows + 31) // 32) / launches_per_step)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    fitter.close()
 
 
 if __name__ == "__main__":

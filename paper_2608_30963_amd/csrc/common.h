@@ -84,6 +84,14 @@ __device__ __forceinline__ void rope_cs(double f, int32_t pos, float& c, float& 
   c = __builtin_amdgcn_cosf(x);
 }
 
+// Workgroup id -> position in XCD-major order: workgroups are dealt
+// round-robin to the 8 XCDs, so this makes each XCD own one contiguous range.
+__device__ __forceinline__ int xcd_remap(int id, int total) {
+  const int q = total / 8, r = total % 8;
+  const int x = id % 8, slot = id / 8;
+  return x * q + min(x, r) + slot;
+}
+
 // Which context a linear row-tile index belongs to (batch is small).
 __device__ __forceinline__ int find_context(const BatchArgs& ba, int tile) {
   int b = 0;

@@ -17,7 +17,9 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
+#include <utility>
 #include <new>
 #include <vector>
 
@@ -216,23 +218,26 @@ __device__ __forceinline__ void prepare_rows(const PrepArgs& a, int job, int r0,
 struct GramArgs {
   const bf16_t* xt;   // [sys][2][F][rp]
   float* acc;         // [sys_total][din_p][F]; this group starts at sys0
-  int32_t F, rp, nbi, nbj, sys0;
+  int32_t F, rp, nbi, nbj, sys0, nblk;
 };
 
 // One workgroup: one 128 x 128 block (bi, bj >= bi) of one system, all rows.
+// Work items are system-major and each XCD takes a contiguous range, so the
+// workgroups that re-read one system's operands share that XCD's L2.
 // Four waves in 2 x 2, each 64 x 64 (2 x 2 MFMA tiles).  Slabs of 32 rows of
 // both feature blocks (hi and lo planes) are staged through LDS, double
 // buffered; the next slab is loaded into registers during the MFMAs.
 __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sl[2][2][2][kFB * kPitch];  // [stage][A|B][plane]
-  int x = blockIdx.x;
+  const int wid = xcd_remap(blockIdx.x, gridDim.x);
+  const int sys = wid / a.nblk;
+  int x = wid % a.nblk;
   int bi = 0;
   while (x >= a.nbj - bi) {
     x -= a.nbj - bi;
     ++bi;
   }
   const int bj = bi + x;
-  const int sys = blockIdx.y;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
@@ -242,9 +247,11 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
 
   // loader: piece p = tid + 256 * u (u < 2) of a 128-feature x 32-row slab
   // plane: feature p / 4, 16-byte column p % 4; 2 blocks x 2 planes x 2.
+  // Two register sets: the loads of slab s + 2 are issued before the MFMAs
+  // of slab s, so they have about two slabs of compute to arrive.
   typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-  u32x4 ld[2][2][2];
-  auto load_slab = [&](int r0) __attribute__((always_inline)) {
+  u32x4 ld[2][2][2][2];  // [set][A|B][plane][u]
+  auto load_slab = [&](int set, int r0) __attribute__((always_inline)) {
 #pragma unroll
     for (int ab = 0; ab < 2; ++ab)
 #pragma unroll
@@ -253,12 +260,11 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
         for (int u = 0; u < 2; ++u) {
           const int p = tid + 256 * u;
           const int f = (ab ? bj : bi) * kFB + p / 4;
-          ld[ab][pl][u] = *reinterpret_cast<const u32x4*>(xs + pl * plane +
-                                                          static_cast<int64_t>(f) * a.rp + r0 +
-                                                          (p % 4) * 8);
+          ld[set][ab][pl][u] = *reinterpret_cast<const u32x4*>(
+              xs + pl * plane + static_cast<int64_t>(f) * a.rp + r0 + (p % 4) * 8);
         }
   };
-  auto store_slab = [&](int st) __attribute__((always_inline)) {
+  auto store_slab = [&](int set, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int ab = 0; ab < 2; ++ab)
 #pragma unroll
@@ -267,7 +273,7 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
         for (int u = 0; u < 2; ++u) {
           const int p = tid + 256 * u;
           *reinterpret_cast<u32x4*>(&sl[st][ab][pl][(p / 4) * kPitch + (p % 4) * 8]) =
-              ld[ab][pl][u];
+              ld[set][ab][pl][u];
         }
   };
 
@@ -280,12 +286,14 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const int nslab = a.rp / kSlab;
-  load_slab(0);
-  store_slab(0);
+  load_slab(0, 0);
+  store_slab(0, 0);
+  if (nslab > 1) load_slab(1, kSlab);
   __syncthreads();
-  for (int s = 0; s < nslab; ++s) {
+  // slab s: computed from LDS stage s % 2, loaded into register set s % 2
+  auto body = [&](int s, int set) __attribute__((always_inline)) {
     const int st = s % 2;
-    if (s + 1 < nslab) load_slab((s + 1) * kSlab);
+    if (s + 2 < nslab) load_slab(set, (s + 2) * kSlab);
 #pragma unroll
     for (int ks = 0; ks < kSlab / 16; ++ks) {
       bf16x8 fa[2][2], fb[2][2];
@@ -298,20 +306,25 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
           fb[t][pl] = *reinterpret_cast<const bf16x8*>(
               &sl[st][1][pl][(wj * 64 + t * 32 + lane % 32) * kPitch + ks * 16 + 8 * (lane / 32)]);
         }
+      // hi*hi, hi*lo, lo*hi; consecutive MFMAs use different accumulators
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int term = 0; term < 3; ++term)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i][0], fb[j][0], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i][0], fb[j][1], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i][1], fb[j][0], acc[i][j], 0, 0, 0);
-        }
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                fa[i][term == 2 ? 1 : 0], fb[j][term == 1 ? 1 : 0], acc[i][j], 0, 0, 0);
     }
-    if (s + 1 < nslab) {
-      store_slab(st ^ 1);
-    }
+    if (s + 1 < nslab) store_slab(set ^ 1, st ^ 1);
     __syncthreads();
+  };
+  int s = 0;
+  for (; s + 1 < nslab; s += 2) {
+    body(s, 0);
+    body(s + 1, 1);
   }
+  if (s < nslab) body(s, 0);
   // D register v of lane l: row 8*(v/4) + 4*(l/32) + v%4, column l%32
   float* out = a.acc + static_cast<int64_t>(a.sys0 + sys) * (a.nbi * kFB) * a.F;
 #pragma unroll
@@ -431,20 +444,89 @@ __global__ void __launch_bounds__(256) fit_solve(SolveArgs a) {
   if (bad) a.status[0] = 1;
   __syncthreads();
 
-  // forward: L Y = B (columns c in parallel)
-  for (int c = tid; c < m; c += 256) {
-    for (int i = 0; i < n; ++i) {
-      const double* li = A + static_cast<int64_t>(i) * n;
-      double s = X[static_cast<int64_t>(i) * m + c];
-      for (int p = 0; p < i; ++p) s -= li[p] * X[static_cast<int64_t>(p) * m + c];
-      X[static_cast<int64_t>(i) * m + c] = s / li[i];
+  // L Y = B, then L^T X = Y, blocked: each thread owns one right-hand side
+  // column (chunks of 256 columns); the 32 unknowns of the current block
+  // live in registers and the L tiles they need are staged in LDS.
+  for (int c0 = 0; c0 < m; c0 += 256) {
+    const int c = c0 + tid;
+    const bool on = c < m;
+    double y[kNB];
+    // forward
+    for (int kb = 0; kb < n; kb += kNB) {
+      const int kw = min(kNB, n - kb);
+      for (int idx = tid; idx < kNB * kNB; idx += 256) {
+        const int i = idx / kNB, j = idx % kNB;
+        pk[i][j] = (i < kw && j <= i) ? A[static_cast<int64_t>(kb + i) * n + kb + j] : 0.0;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < kNB; ++q) {
+        double v = 0.0;
+        if (on && q < kw) {
+          v = X[static_cast<int64_t>(kb + q) * m + c];
+#pragma unroll
+          for (int p = 0; p < q; ++p) v -= pk[q][p] * y[p];
+          v /= pk[q][q];
+          X[static_cast<int64_t>(kb + q) * m + c] = v;
+        }
+        y[q] = v;
+      }
+      for (int i0 = kb + kw; i0 < n; i0 += kNB) {
+        __syncthreads();
+        for (int idx = tid; idx < kNB * kNB; idx += 256) {
+          const int r = idx / kNB, q = idx % kNB;
+          pr[r][q] = (i0 + r < n && q < kw) ? A[static_cast<int64_t>(i0 + r) * n + kb + q] : 0.0;
+        }
+        __syncthreads();
+        if (on)
+          for (int r = 0; r < kNB && i0 + r < n; ++r) {
+            double v = X[static_cast<int64_t>(i0 + r) * m + c];
+#pragma unroll
+            for (int q = 0; q < kNB; ++q) v -= pr[r][q] * y[q];
+            X[static_cast<int64_t>(i0 + r) * m + c] = v;
+          }
+      }
+      __syncthreads();
     }
-    // backward: L^T X = Y
-    for (int i = n - 1; i >= 0; --i) {
-      double s = X[static_cast<int64_t>(i) * m + c];
-      for (int p = i + 1; p < n; ++p)
-        s -= A[static_cast<int64_t>(p) * n + i] * X[static_cast<int64_t>(p) * m + c];
-      X[static_cast<int64_t>(i) * m + c] = s / A[static_cast<int64_t>(i) * n + i];
+    // backward
+    const int nblk = (n + kNB - 1) / kNB;
+    for (int bk = nblk - 1; bk >= 0; --bk) {
+      const int kb = bk * kNB;
+      const int kw = min(kNB, n - kb);
+      for (int idx = tid; idx < kNB * kNB; idx += 256) {
+        const int i = idx / kNB, j = idx % kNB;
+        pk[i][j] = (i < kw && j <= i) ? A[static_cast<int64_t>(kb + i) * n + kb + j] : 0.0;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int q = kNB - 1; q >= 0; --q) {
+        double v = 0.0;
+        if (on && q < kw) {
+          v = X[static_cast<int64_t>(kb + q) * m + c];
+#pragma unroll
+          for (int p = q + 1; p < kNB; ++p) v -= (p < kw ? pk[p][q] * y[p] : 0.0);
+          v /= pk[q][q];
+          X[static_cast<int64_t>(kb + q) * m + c] = v;
+        }
+        y[q] = v;
+      }
+      // rows above: X[i] -= sum_q L[kb + q][i] x_q
+      for (int i0 = 0; i0 < kb; i0 += kNB) {
+        __syncthreads();
+        for (int idx = tid; idx < kNB * kNB; idx += 256) {
+          const int q = idx / kNB, r = idx % kNB;
+          pr[r][q] = q < kw ? A[static_cast<int64_t>(kb + q) * n + i0 + r] : 0.0;
+        }
+        __syncthreads();
+        if (on)
+          for (int r = 0; r < kNB; ++r) {
+            double v = X[static_cast<int64_t>(i0 + r) * m + c];
+#pragma unroll
+            for (int q = 0; q < kNB; ++q) v -= pr[r][q] * y[q];
+            X[static_cast<int64_t>(i0 + r) * m + c] = v;
+          }
+      }
+      __syncthreads();
     }
   }
   __syncthreads();
@@ -495,6 +577,7 @@ struct kvx_fit {
   void* solve_buf = nullptr;
   size_t solve_bytes = 0;
   int64_t rows = 0;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> timed;  // KVX_FIT_TIMING=1
 };
 
 extern "C" {
@@ -606,6 +689,8 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
     return KVX_ESHAPE;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int esz = f->dtype == KVX_F32 ? 4 : 2;
+  const char* tenv = std::getenv("KVX_FIT_TIMING");
+  const bool timing = tenv && tenv[0] == '1';
 
   int64_t row_base = 0;
   for (int64_t b0 = 0; b0 < B; b0 += kFitBatch) {
@@ -688,8 +773,19 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
       ga.sys0 = static_cast<int32_t>(l0 * 2);
       int nblk = 0;
       for (int bi = 0; bi < ga.nbi; ++bi) nblk += ga.nbj - bi;
-      fit_gram<<<dim3(nblk, nl * 2), dim3(256), 0, st>>>(ga);
+      ga.nblk = nblk;
+      hipEvent_t ev[2] = {nullptr, nullptr};
+      if (timing) {
+        FIT_HIP(hipEventCreate(&ev[0]));
+        FIT_HIP(hipEventCreate(&ev[1]));
+        FIT_HIP(hipEventRecord(ev[0], st));
+      }
+      fit_gram<<<dim3(nblk * nl * 2), dim3(256), 0, st>>>(ga);
       FIT_HIP(hipGetLastError());
+      if (timing) {
+        FIT_HIP(hipEventRecord(ev[1], st));
+        f->timed.emplace_back(ev[0], ev[1]);
+      }
     }
   }
   f->rows += rows;
@@ -752,8 +848,39 @@ kvx_status kvx_fit_reset(kvx_fit* f, void* stream) {
 
 int64_t kvx_fit_rows(const kvx_fit* f) { return f ? f->rows : 0; }
 
+kvx_status kvx_fit_query(kvx_fit* f, kvx_fit_info* info) {
+  if (!f || !info) return KVX_EINVAL;
+  *info = kvx_fit_info{};
+  info->systems = 2 * f->tgt.n_layers;
+  info->n = f->n;
+  const int nbi = f->din_p / kFB, nbj = f->F / kFB;
+  for (int bi = 0; bi < nbi; ++bi) info->gram_blocks += nbj - bi;
+  info->rows = f->rows;
+  info->device_bytes = static_cast<int64_t>(size_t(f->tgt.n_layers) * 2 * f->din_p * f->F *
+                                            sizeof(float) + f->scratch_bytes + f->solve_bytes);
+  double ms = 0.0;
+  kvx_status rc = KVX_OK;
+  for (auto& p : f->timed) {
+    float t = 0.f;
+    hipError_t e = hipEventSynchronize(p.second);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, p.first, p.second);
+    if (e != hipSuccess) rc = fit_hip_fail(e);
+    ms += t;
+    (void)hipEventDestroy(p.first);
+    (void)hipEventDestroy(p.second);
+  }
+  info->gram_launches = static_cast<int32_t>(f->timed.size());
+  info->gram_ms = ms;
+  f->timed.clear();
+  return rc;
+}
+
 void kvx_fit_destroy(kvx_fit* f) {
   if (!f) return;
+  for (auto& p : f->timed) {
+    (void)hipEventDestroy(p.first);
+    (void)hipEventDestroy(p.second);
+  }
   if (f->layer_map) (void)hipFree(f->layer_map);
   if (f->fs) (void)hipFree(f->fs);
   if (f->ft) (void)hipFree(f->ft);

@@ -88,14 +88,6 @@ constexpr int fused_lds_bytes() { return 2 * 2 * kPlane * 2; }
 constexpr int kMaxLayerMap = 1024;  // target layers * mix held in LDS
 constexpr int kMaxHalfDim = 256;    // source head_dim / 2 held in LDS
 
-// Workgroup id -> position in XCD-major order: workgroups are dealt
-// round-robin to the 8 XCDs, so this makes each XCD own one contiguous range.
-__device__ __forceinline__ int xcd_remap(int id, int total) {
-  const int q = total / 8, r = total % 8;
-  const int x = id % 8, slot = id / 8;
-  return x * q + min(x, r) + slot;
-}
-
 struct Tile {
   int l, kv, nt, b, t0, tt, rb;
 };

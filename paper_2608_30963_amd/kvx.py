@@ -28,7 +28,8 @@ KVX_PREC_BF16X2, KVX_PREC_BF16, KVX_PREC_F16 = 0, 1, 2
 # Exported C symbols, as declared in include/kvx.h and include/kvx_fit.h.
 SYMBOLS = ("kvx_plan_create", "kvx_translate", "kvx_plan_destroy", "kvx_status_string",
            "kvx_last_hip_error", "kvx_plan_query", "kvx_fit_create", "kvx_fit_accumulate",
-           "kvx_fit_solve", "kvx_fit_reset", "kvx_fit_rows", "kvx_fit_destroy")
+           "kvx_fit_solve", "kvx_fit_reset", "kvx_fit_rows", "kvx_fit_query",
+           "kvx_fit_destroy")
 
 
 class KvxError(RuntimeError):
@@ -73,6 +74,12 @@ class FitIO(C.Structure):
                 ("tgt_capacity", C.c_int32)]
 
 
+class FitInfo(C.Structure):
+    _fields_ = [("systems", C.c_int32), ("n", C.c_int32), ("gram_blocks", C.c_int32),
+                ("gram_launches", C.c_int32), ("rows", C.c_int64),
+                ("device_bytes", C.c_int64), ("gram_ms", C.c_double)]
+
+
 class PlanInfo(C.Structure):
     _fields_ = [("kernel", C.c_int32), ("tile_rows", C.c_int32), ("tile_cols", C.c_int32),
                 ("threads", C.c_int32), ("precision", C.c_int32), ("weight_bytes", C.c_int64)]
@@ -112,6 +119,8 @@ def load(path: str = LIB_PATH):
     lib.kvx_fit_reset.restype = C.c_int
     lib.kvx_fit_rows.argtypes = [C.c_void_p]
     lib.kvx_fit_rows.restype = C.c_int64
+    lib.kvx_fit_query.argtypes = [C.c_void_p, C.POINTER(FitInfo)]
+    lib.kvx_fit_query.restype = C.c_int
     lib.kvx_fit_destroy.argtypes = [C.c_void_p]
     lib.kvx_fit_destroy.restype = None
     _lib = lib
@@ -337,6 +346,14 @@ def kvx_fit_rows(fit: int) -> int:
     return int(load().kvx_fit_rows(C.c_void_p(fit)))
 
 
+def kvx_fit_query(fit: int) -> FitInfo:
+    info = FitInfo()
+    st = load().kvx_fit_query(C.c_void_p(fit), C.byref(info))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_fit_query")
+    return info
+
+
 def kvx_fit_destroy(fit: Optional[int]) -> None:
     load().kvx_fit_destroy(C.c_void_p(fit) if fit else None)
 
@@ -382,6 +399,9 @@ class Fitter:
     @property
     def rows(self) -> int:
         return kvx_fit_rows(self.handle)
+
+    def info(self) -> FitInfo:
+        return kvx_fit_query(self.handle)
 
     def close(self):
         if self.handle:

@@ -23,6 +23,8 @@ independently):
     (seed, cfg, 6, b)         span lengths of context b
     (seed, cfg, 7, l)         bias of K (only when bias_std > 0)
     (seed, cfg, 8, l)         bias of V
+    (seed, cfg, 9, l, b)      native target K of the fit (draw_native_target)
+    (seed, cfg, 10, l, b)     native target V of the fit
 
 Values are drawn in float32 and then cast round-to-nearest-even to the
 storage dtype; bf16 tensors are returned as their uint16 bit patterns.
@@ -335,6 +337,22 @@ def make_problem(spec: Spec, src_layers=None) -> Problem:
     return Problem(spec, src_k, src_v, w_k, w_v, draw_bias(spec, 0), draw_bias(spec, 1),
                    tgt_tokens, row_ptr, col_idx, weight,
                    np.asarray(spec.layer_map, dtype=np.int32))
+
+
+def draw_native_target(spec: Spec, which: int, tgt_tokens) -> np.ndarray:
+    """Stand-in for a target model's own prefill cache, K (which=0) or V
+    (which=1): N(0, 1) rows [Lt, B, Ht, cap, Dt] in the storage dtype, rows
+    past a context's T_t zero.  Streams (seed, cfg, 9 + which, l, b)."""
+    t = spec.tgt
+    tt = np.asarray(tgt_tokens)
+    cap = int(tt.max()) if len(tt) else 0
+    out = np.zeros((t.n_layers, spec.batch, t.n_kv_heads, cap, t.head_dim), dtype=np.float32)
+    for l in range(t.n_layers):
+        for b in range(spec.batch):
+            n = int(tt[b])
+            out[l, b, :, :n] = _rng(spec, 9 + which, l, b).standard_normal(
+                (t.n_kv_heads, n, t.head_dim), dtype=np.float32)
+    return to_storage(out, spec.dtype)
 
 
 def tiny_spec(**kw) -> Spec:

@@ -151,4 +151,6 @@ def test_fit_calls_reject_null():
     assert lib.kvx_fit_solve(None, 1.0, 0x10, 0x10, 0x10, 0x10, None) == kvx.KVX_EINVAL
     assert lib.kvx_fit_reset(None, None) == kvx.KVX_EINVAL
     assert lib.kvx_fit_rows(None) == 0
+    info = kvx.FitInfo()
+    assert lib.kvx_fit_query(None, C.byref(info)) == kvx.KVX_EINVAL
     kvx.kvx_fit_destroy(None)
