@@ -62,9 +62,12 @@ KERNEL_SOURCES = os.path.join(ROOT, "paper_2608_30963_amd", "csrc")
 
 
 def kernel_source_hash() -> str:
-    """sha256 over the HIP sources (file names and contents, sorted)."""
+    """sha256 over the translation's HIP sources (file names and contents,
+    sorted; the translator fit's source is not part of the translation)."""
     h = hashlib.sha256()
     for f in sorted(glob.glob(os.path.join(KERNEL_SOURCES, "*"))):
+        if os.path.basename(f) == "fit.hip":
+            continue
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
             h.update(fh.read())

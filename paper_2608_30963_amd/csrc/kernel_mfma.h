@@ -89,7 +89,7 @@ constexpr int kMaxLayerMap = 1024;  // target layers * mix held in LDS
 constexpr int kMaxHalfDim = 256;    // source head_dim / 2 held in LDS
 
 struct Tile {
-  int l, kv, nt, b, t0, tt, rb;
+  int l, kv, nt, b, t0, tt, rb, rt;
 };
 
 // Tile order: layer slowest, then row tile, then N tile, K|V fastest (so a
@@ -101,12 +101,44 @@ __device__ __forceinline__ Tile decode_tile(const FusedArgs& a, int tau) {
   T.nt = rest % a.n_tiles;
   rest /= a.n_tiles;
   const int rt = rest % a.row_tiles;
+  T.rt = rt;
   T.l = rest / a.row_tiles;
   T.b = find_context(a.ba, rt);
   T.t0 = (rt - a.ba.tile_start[T.b]) * kMT;
   T.tt = a.ba.t_tgt[T.b];
   T.rb = a.ba.row_base[T.b];
   return T;
+}
+
+// The launch's context table, copied to LDS at kernel start so the step
+// loop can index it (a dynamic index into the kernel argument would make the
+// compiler copy the whole argument block to scratch memory).
+struct CtxTable {
+  int32_t tile_start[kMaxBatch + 1];
+  int32_t t_tgt[kMaxBatch];
+  int32_t row_base[kMaxBatch];
+};
+
+// The tile after T in the same order, without divisions.
+__device__ __forceinline__ void advance_tile(int n_tiles, int row_tiles, int n_ctx,
+                                             const CtxTable& cx, Tile& T) {
+  if (T.kv == 0) {
+    T.kv = 1;
+    return;
+  }
+  T.kv = 0;
+  if (++T.nt < n_tiles) return;
+  T.nt = 0;
+  if (++T.rt == row_tiles) {
+    T.rt = 0;
+    ++T.l;
+    T.b = 0;
+  }
+  // uniform values: keep them in scalar registers
+  while (T.b + 1 < n_ctx && __builtin_amdgcn_readfirstlane(cx.tile_start[T.b + 1]) <= T.rt) ++T.b;
+  T.t0 = (T.rt - __builtin_amdgcn_readfirstlane(cx.tile_start[T.b])) * kMT;
+  T.tt = __builtin_amdgcn_readfirstlane(cx.t_tgt[T.b]);
+  T.rb = __builtin_amdgcn_readfirstlane(cx.row_base[T.b]);
 }
 
 // Workgroup barrier that orders LDS only: waits for this wave's LDS (and
@@ -190,27 +222,13 @@ __device__ __forceinline__ void residual8(const float* z, const uint4 hi, float*
   for (int i = 0; i < 8; ++i) r[i] = z[i] - h[i];
 }
 
-// First members of the 8-pair group `grp` (pairs 8*grp .. 8*grp+7 of the
-// flattened (j, h, d) list) at token 0; second members at p + ds/2.
+// First members of an 8-pair group (8 consecutive pairs of the flattened
+// (j, h, d) list) at token 0; second members at p + ds/2.
 struct PairGroup {
   const bf16_t* p;
   int i0;  // frequency index of the first pair
 };
 
-__device__ __forceinline__ PairGroup pair_group(const FusedArgs& a, const int32_t* lmap,
-                                                const bf16_t* src, int l, int b, int grp) {
-  const int half = a.ds / 2;
-  const int pair = grp * 8;
-  const int head_pairs = pair / half;  // (j, h) flattened
-  const int i0 = pair % half;
-  const int j = head_pairs / a.hs;
-  const int h = head_pairs % a.hs;
-  const int ls = lmap[l * a.mix + j];
-  PairGroup g;
-  g.p = src + ls * a.ss.l + b * a.ss.b + h * a.ss.h + i0;
-  g.i0 = i0;
-  return g;
-}
 
 // Alignment entries of the units of one producer thread within one tile.
 struct RowInfo {
@@ -323,6 +341,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   __shared__ float2 rot32[kMaxHalfDim];
   // bias of the tile being finished, in staging-column order (tile parity)
   __shared__ __attribute__((aligned(16))) float biasl[2][kNT];
+  __shared__ CtxTable ctx;
 
   const int G = gridDim.x;
   const int wid = xcd_remap(blockIdx.x, G);
@@ -335,6 +354,15 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   if (nsteps == 0) return;
   const int tid = threadIdx.x;
   for (int i = tid; i < a.lt * a.mix; i += kThreads) lmap[i] = a.layer_map[i];
+  for (int i = tid; i <= a.ba.n; i += kThreads) {
+    ctx.tile_start[i] = a.ba.tile_start[i];
+    if (i < a.ba.n) {
+      ctx.t_tgt[i] = a.ba.t_tgt[i];
+      ctx.row_base[i] = a.ba.row_base[i];
+    }
+  }
+  const int n_tiles = a.n_tiles, row_tiles = a.row_tiles, n_ctx = a.ba.n;
+  auto next_tile = [&](Tile& T) KVX_INLINE { advance_tile(n_tiles, row_tiles, n_ctx, ctx, T); };
   for (int i = tid; i < a.ds / 2; i += kThreads) fsl[i] = a.fs[i];
   for (int i = tid; i < a.dt / 2; i += kThreads) {
     ftl[i] = a.ft[i];
@@ -387,21 +415,66 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       RowInfo ri;
     };
     Raw rA, rB, rC;
-    int f_tile = -1;
-    Tile ftile{};
-    RowInfo fri;
-    // Address of chunk cs's first 8-pair group for this thread (and the tile's
-    // row info).  Done before the step's LDS writes: its LDS and scalar
-    // lookups then do not wait for those writes to drain.
-    auto fetch_addr = [&](int cs) KVX_INLINE -> const bf16_t* {
-      const int tau = tbeg + cs / nch;
-      const int c = cs % nch;
-      if (tau != f_tile) {
-        f_tile = tau;
-        ftile = decode_tile(a, tau);
-        if (!IDENT) row_info(ftile, fri);
+    // This thread's 8-pair group at chunk 0 of any tile: mixed layer j0,
+    // source head h0, first frequency i00 (pair 8 g of the flattened list).
+    const int half = a.ds / 2;
+    const int hp0 = (8 * g) / half;
+    const int j0 = hp0 / a.hs, h0 = hp0 % a.hs, i00 = (8 * g) % half;
+    // Position of a chunk: its tile, chunk index in the tile, this thread's
+    // group; advanced one chunk at a time (no divisions in the step loop).
+    struct ChunkPos {
+      Tile T;
+      int c, j, h, i0, ord;  // ord: tile ordinal within this workgroup's range
+    };
+    auto advance_pos = [&](ChunkPos& P) KVX_INLINE {
+      if (++P.c == nch) {
+        P.c = 0;
+        ++P.ord;
+        if (P.ord < tend - tbeg) next_tile(P.T);
+        P.j = j0;
+        P.h = h0;
+        P.i0 = i00;
+        return;
       }
-      return pair_group(a, lmap, a.src[ftile.kv], ftile.l, ftile.b, c * 8 + g).p;
+      P.i0 += 64;  // a chunk holds 64 pairs
+      while (P.i0 >= half) {
+        P.i0 -= half;
+        if (++P.h == a.hs) {
+          P.h = 0;
+          ++P.j;
+        }
+      }
+    };
+    auto group_ptr = [&](const ChunkPos& P) KVX_INLINE -> const bf16_t* {
+      const int ls = lmap[P.T.l * a.mix + P.j];
+      return a.src[P.T.kv] + ls * a.ss.l + P.T.b * a.ss.b + P.h * a.ss.h + P.i0;
+    };
+    ChunkPos fpos;
+    fpos.T = decode_tile(a, tbeg);
+    fpos.c = 0;
+    fpos.j = j0;
+    fpos.h = h0;
+    fpos.i0 = i00;
+    fpos.ord = 0;
+    ChunkPos tpos = fpos;  // transform position
+    Tile ftile = fpos.T;
+    RowInfo fri;
+    const bf16_t* fgp = nullptr;
+    // Address of the next chunk's first 8-pair group for this thread (and
+    // the tile's row info); `more` false: no further chunk, the previous
+    // address is returned (its loads read the zero sink).  Done before the
+    // step's LDS writes: its LDS and scalar lookups then do not wait for
+    // those writes to drain.
+    auto fetch_addr = [&](bool more) KVX_INLINE -> const bf16_t* {
+      if (more) {
+        if (fpos.c == 0) {
+          ftile = fpos.T;
+          if (!IDENT) row_info(ftile, fri);
+        }
+        fgp = group_ptr(fpos);
+        advance_pos(fpos);
+      }
+      return fgp;
     };
     // `more` false: there is no such chunk; the loads still issue (from the
     // zero sink), so every step issues the same loads.
@@ -423,10 +496,10 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
 
     float csc[CS_CACHE ? kUnits : 1][8], css[CS_CACHE ? kUnits : 1][8];
 
-    auto transform = [&](int cs, const Raw& R, bf16_t* hi, bf16_t* lo) KVX_INLINE {
-      const int tau = tbeg + cs / nch;
-      const int c = cs % nch;
-      const Tile T = decode_tile(a, tau);
+    // Transform the chunk at tpos (chunks are transformed in order).
+    auto transform = [&](const Raw& R, bf16_t* hi, bf16_t* lo) KVX_INLINE {
+      const Tile T = tpos.T;
+      const int c = tpos.c;
       const bool is_k = T.kv == 0;
       if (IDENT && !is_k && PREC != kF16) {
         // identity-aligned V: the bf16 source rows are the operand
@@ -436,9 +509,12 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
           *reinterpret_cast<uint4*>(hi + r * kLDA + 8 * g) = R.x0[u];
           *reinterpret_cast<uint4*>(hi + r * kLDA + 64 + 8 * g) = R.x1[u];
         }
+        advance_pos(tpos);
         return;
       }
-      const PairGroup pg = pair_group(a, lmap, a.src[T.kv], T.l, T.b, c * 8 + g);
+      PairGroup pg;
+      pg.p = group_ptr(tpos);
+      pg.i0 = tpos.i0;
       double f[8];
       if (is_k && (!CS_CACHE || c == 0)) {
 #pragma unroll
@@ -517,28 +593,32 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
           *reinterpret_cast<uint4*>(lo + r * kLDA + 64 + 8 * g) = pack8(d1);
         }
       }
+      advance_pos(tpos);
     };
 
-    // chunk cs is consumed at step s(cs) = (cs / nch) * spt + cs % nch and
-    // written into buffer s(cs) % 2 during the step before.
-    auto step_of = [&](int cs) KVX_INLINE { return (cs / nch) * spt + cs % nch; };
-    fetch_issue(fetch_addr(0), rA, true);
-    fetch_issue(fetch_addr(nchunks > 1 ? 1 : 0), rB, nchunks > 1);
-    if constexpr (kDepth == 3) fetch_issue(fetch_addr(nchunks > 2 ? 2 : 0), rC, nchunks > 2);
+    // chunk cs is consumed at step (its tile ordinal) * spt + (its index in the
+    // tile) and written into that step's buffer during the step before.
+    fetch_issue(fetch_addr(true), rA, true);
+    fetch_issue(fetch_addr(nchunks > 1), rB, nchunks > 1);
+    if constexpr (kDepth == 3) fetch_issue(fetch_addr(nchunks > 2), rC, nchunks > 2);
     {
-      const bf16_t* gp = fetch_addr(nchunks > kDepth ? kDepth : 0);
-      transform(0, rA, lds, lds + kPlane);
+      const bf16_t* gp = fetch_addr(nchunks > kDepth);
+      transform(rA, lds, lds + kPlane);
       fetch_issue(gp, rA, nchunks > kDepth);
     }
     lds_barrier();
-    // Step s ends with a barrier; in an epilogue step (s % spt == nch) the
-    // consumers have staged the finished tile in buffer s % 2 at its middle
-    // barrier and the producers then write its rows (the consumers issue no
-    // global stores, so their weight loads never wait behind stores).
+    // Step s ends with a barrier; in an epilogue step (sc == nch) the
+    // consumers stage the finished tile in buffer s % 2 and the producers
+    // write its rows (the consumers issue no global stores, so their weight
+    // loads never wait behind stores).
     int s = 0;
-    // physical blocks of this thread's rows of the next tile to be stored
+    int sc = 0;    // s % spt
+    int sord = 0;  // s / spt: tile ordinal of step s
+    // tile whose rows are stored next, and the physical blocks of its rows
+    Tile stT = decode_tile(a, tbeg);
+    int st_ord = 0;
     int32_t blk[kRowsPerThread];
-    load_blocks<PAGED>(a, decode_tile(a, tbeg), tid, blk);
+    load_blocks<PAGED>(a, stT, tid, blk);
     // Bias entry `tid` of a tile in staging-column order (consumer wave
     // tid / 64, block tid / 32 % 2, feature tid % 32); pair blocks past dout
     // read the zero sink.
@@ -553,39 +633,51 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     };
     // tile 0's bias now; each later tile's is loaded during the previous
     // tile's epilogue step and written at the end of its own first step
-    biasl[0][tid] = bias_entry(decode_tile(a, tbeg));
-    float bias_next = bias_entry(decode_tile(a, tbeg + 1 < tend ? tbeg + 1 : tbeg));
-    // Rows of tile tau staged in buffer sb, then the block ids of the next.
-    auto store_tile = [&](int tau, int sb) KVX_INLINE {
-      store_rows<PAGED>(a, decode_tile(a, tau), lds + sb * 2 * kPlane, tid, blk);
-      load_blocks<PAGED>(a, decode_tile(a, tau + 1 < tend ? tau + 1 : tau), tid, blk);
+    biasl[0][tid] = bias_entry(stT);
+    // at the epilogue step of tile k, biasT becomes tile k + 1 (the last
+    // tile repeats itself) and its bias is loaded
+    Tile biasT = stT;
+    int bias_ord = 0;
+    float bias_next = 0.f;
+    // Rows of tile stT staged in buffer sb, then the block ids of the next.
+    auto store_tile = [&](int sb) KVX_INLINE {
+      store_rows<PAGED>(a, stT, lds + sb * 2 * kPlane, tid, blk);
+      if (++st_ord < tend - tbeg) next_tile(stT);
+      load_blocks<PAGED>(a, stT, tid, blk);
     };
     auto end_step = [&]() KVX_INLINE {
-      if (s % spt == 0 && s > 0) biasl[(s / spt) % 2][tid] = bias_next;
-      if (s % spt == nch) {
-        const int tau = tbeg + s / spt;
+      if (sc == 0 && s > 0) biasl[sord & 1][tid] = bias_next;
+      if (sc == nch) {
         if (!kDeferStores) {
           lds_barrier();  // staging complete
-          store_tile(tau, s % 2);
+          store_tile(s & 1);
         }
-        bias_next = bias_entry(decode_tile(a, tau + 1 < tend ? tau + 1 : tau));
+        if (bias_ord + 1 < tend - tbeg) {
+          next_tile(biasT);
+          ++bias_ord;
+        }
+        bias_next = bias_entry(biasT);
       }
       lds_barrier();
       ++s;
+      if (++sc == spt) {
+        sc = 0;
+        ++sord;
+      }
       // deferred: the tile staged in step s - 1, before this thread's
       // transform of step s reuses the slots
-      if (kDeferStores && s % spt == 0) store_tile(tbeg + s / spt - 1, (s - 1) % 2);
+      if (kDeferStores && sc == 0) store_tile((s - 1) & 1);
     };
-    // Transform chunk `next` (consumed at step step_of(next)) during the step
-    // before it, from raw set R, and refill R with chunk next + kDepth.
-    // Called with the sets in turn (chunk mod kDepth), so each set keeps its
-    // registers.
+    // Transform the next chunk (the one at tpos, consumed at step
+    // tpos.ord * spt + tpos.c) during the step before it, from raw set R, and
+    // refill R with the chunk kDepth further on.  Called with the sets in turn
+    // (chunk mod kDepth), so each set keeps its registers.
     auto produce = [&](int next, Raw& R) KVX_INLINE {
-      while (s + 1 < step_of(next)) end_step();  // steps with nothing to transform
-      bf16_t* buf = lds + ((s + 1) % 2) * 2 * kPlane;
+      while (s + 1 < tpos.ord * spt + tpos.c) end_step();  // steps with nothing to transform
+      bf16_t* buf = lds + ((s + 1) & 1) * 2 * kPlane;
       const bool more = next + kDepth < nchunks;
-      const bf16_t* gp = fetch_addr(more ? next + kDepth : next);
-      transform(next, R, buf, buf + kPlane);
+      const bf16_t* gp = fetch_addr(more);
+      transform(R, buf, buf + kPlane);
       fetch_issue(gp, R, more);
       end_step();
     };
@@ -621,23 +713,28 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   const int fq = 4 * (lane / 32);
 
   struct Blocks {
-    int on;
+    int on, nt;
     int c0, c1, q, hp;
     const bf16x8* w0p;
     const bf16x8* w1p;
   };
+  // weight fragment pointers of blocks c0 / c1 for tile T's layer and K|V
+  auto rebase = [&](Blocks& B, const Tile& T) KVX_INLINE {
+    const bf16x8* wsel = PREC == kF16 ? a.wh[T.kv] : a.wp[T.kv];
+    const bf16x8* base = wsel + static_cast<int64_t>(T.l) * (a.dout / 32) * KSALL * 64;
+    B.w0p = base + static_cast<int64_t>(B.c0 / 32) * KSALL * 64 + lane;
+    B.w1p = base + static_cast<int64_t>(B.c1 / 32) * KSALL * 64 + lane;
+  };
   auto blocks = [&](const Tile& T, int w) KVX_INLINE {
     Blocks B;
     const int pb = T.nt * 4 + w;
+    B.nt = T.nt;
     B.on = pb < npb;
     B.hp = B.on ? pb / per_head : 0;
     B.q = B.on ? pb % per_head : 0;
     B.c0 = B.hp * a.dt + 32 * B.q;
     B.c1 = B.c0 + a.dt / 2;
-    const bf16x8* wsel = PREC == kF16 ? a.wh[T.kv] : a.wp[T.kv];
-    const bf16x8* base = wsel + static_cast<int64_t>(T.l) * (a.dout / 32) * KSALL * 64;
-    B.w0p = base + static_cast<int64_t>(B.c0 / 32) * KSALL * 64 + lane;
-    B.w1p = base + static_cast<int64_t>(B.c1 / 32) * KSALL * 64 + lane;
+    rebase(B, T);
     return B;
   };
 
@@ -719,23 +816,27 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   Blocks Bn = B;
   load_w(B, 0);  // valid addresses even for a pair block past dout
   lds_barrier();
-  int cs = 0;  // global chunk index
+  int cs = 0;    // global chunk index
+  int c = 0;     // chunk within the tile; c == nch: epilogue step
+  int tpar = 0;  // tile parity (bias buffer)
   for (int s = 0; s < nsteps; ++s) {
-    bf16_t* buf = lds + (s % 2) * 2 * kPlane;
-    if (s % spt < nch) {
+    bf16_t* buf = lds + (s & 1) * 2 * kPlane;
+    if (c < nch) {
       // ---------------- chunk step ----------------
-      const int c = s % spt;
       const bool computed = T.kv == 0 || !IDENT;
       // weights four k-steps ahead (k-steps 4..7 of this chunk, then 0..3 of
       // the next chunk, possibly of the next tile): a ring slot is reloaded
       // as soon as the MFMAs of its k-step have issued
-      int cn = 0;
       const bool more = cs + 1 < nchunks;
+      const int cn = more && c + 1 < nch ? c + 1 : 0;
       if (c == 0) Bn = B;
-      if (more) {
-        cn = (cs + 1) % nch;
-        if (cn == 0) {
-          Tn = decode_tile(a, tbeg + (cs + 1) / nch);
+      if (more && cn == 0) {
+        Tn = T;
+        next_tile(Tn);
+        if (Tn.nt == B.nt) {
+          Bn = B;
+          rebase(Bn, Tn);
+        } else {
           Bn = blocks(Tn, cw);
         }
       }
@@ -801,16 +902,19 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         load_w(Bn, cn);
       }
       ++cs;
+      ++c;
       lds_barrier();
     } else {
       // ---------------- epilogue step ----------------
-      if (B.on) stage(T, B, buf, biasl[(s / spt) % 2]);
+      if (B.on) stage(T, B, buf, biasl[tpar]);
       lds_barrier();  // staging complete
       if (!kDeferStores) lds_barrier();  // the producers' row stores
       if (cs < nchunks) {
         T = Tn;
         B = Bn;
       }
+      c = 0;
+      tpar ^= 1;
     }
   }
 }
