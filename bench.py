@@ -63,10 +63,11 @@ KERNEL_SOURCES = os.path.join(ROOT, "paper_2608_30963_amd", "csrc")
 
 def kernel_source_hash() -> str:
     """sha256 over the translation's HIP sources (file names and contents,
-    sorted; the translator fit's source is not part of the translation)."""
+    sorted; the translator fit and the plan-time composition of translator
+    variants are not part of the translation launch)."""
     h = hashlib.sha256()
     for f in sorted(glob.glob(os.path.join(KERNEL_SOURCES, "*"))):
-        if os.path.basename(f) == "fit.hip":
+        if os.path.basename(f) in ("fit.hip", "compose.hip"):
             continue
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:

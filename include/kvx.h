@@ -145,6 +145,42 @@ kvx_status kvx_plan_create(const kvx_plan_desc* desc, kvx_plan** out);
  * per-call scratch, so concurrent calls on different streams are safe. */
 kvx_status kvx_translate(const kvx_plan* plan, const kvx_io* io, void* stream);
 
+/* Translator variants, composed on the device into the plan's dense
+ * per-layer W (and b) at plan creation.  Section 5 of the paper lists
+ * low-dimensional latent adapters among the translation mechanisms and
+ * Section 2.2 recalls a mixture of translator modules:
+ *   KVX_FACTORS_LOWRANK  u = U[l] (V[l] z) + b[l]   ->  W[l] = U[l] V[l]
+ *   KVX_FACTORS_MIXTURE  u = sum_k alpha_k (W_k[l] z + b_k[l])
+ *                        ->  W[l] = sum_k alpha_k W_k[l], b[l] = sum_k alpha_k b_k[l]
+ * The composition reads the factors in the plan's dtype, accumulates in fp32
+ * and rounds W once to the plan's dtype (b stays fp32); the translation then
+ * runs as for a dense plan, so the equality with the literal variant holds up
+ * to that one rounding of W. */
+typedef enum { KVX_FACTORS_LOWRANK = 1, KVX_FACTORS_MIXTURE = 2 } kvx_factors_kind;
+
+typedef struct {
+  int32_t kind;            /* kvx_factors_kind */
+  int32_t rank;            /* LOWRANK: r >= 1 */
+  const void* u_k;         /* LOWRANK: device [Lt][Ht*Dt][r], plan dtype */
+  const void* u_v;
+  const void* v_k;         /* LOWRANK: device [Lt][r][mix*Hs*Ds], plan dtype */
+  const void* v_v;
+  int32_t n_mix;           /* MIXTURE: 1 <= K <= 32 */
+  const double* alpha;     /* MIXTURE: host [K], finite */
+  const void* w_k;         /* MIXTURE: device [K][Lt][Ht*Dt][mix*Hs*Ds], plan dtype */
+  const void* w_v;
+  const float* b_k;        /* MIXTURE: device fp32 [K][Lt][Ht*Dt], or NULL for zero */
+  const float* b_v;
+} kvx_factors;
+
+/* As kvx_plan_create, with W (and, for a mixture, b) composed from `f`;
+ * desc->w_k / w_v are not read (may be NULL); desc->b_k / b_v give the bias
+ * of a low-rank plan and are not read for a mixture.  Synchronous.  Errors as
+ * kvx_plan_create, plus KVX_EINVAL for a bad kind, rank, K or alpha and
+ * KVX_EUNSUPPORTED for K > 32. */
+kvx_status kvx_plan_create_factored(const kvx_plan_desc* desc, const kvx_factors* f,
+                                    kvx_plan** out);
+
 /* Release a plan (NULL-safe).  The caller must ensure no translation that uses
  * it is still running. */
 void kvx_plan_destroy(kvx_plan* plan);

@@ -4,12 +4,19 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kvx.h"
+
 namespace kvx {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef uint16_t bf16_t;  // storage: bfloat16 bit pattern
+
+// Status for a HIP call's result: KVX_OK on success, else KVX_ENOMEM or
+// KVX_EHIP with the code recorded for kvx_last_hip_error() of the calling
+// thread.  Host only; defined with the plan functions.
+kvx_status hip_status(hipError_t e);
 
 // Contexts handled by one launch; larger batches are split by the host.
 constexpr int kMaxBatch = 64;

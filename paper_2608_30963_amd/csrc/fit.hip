@@ -36,12 +36,7 @@ constexpr int kPitch = kSlab + 8;  // LDS pitch (bf16) of one feature's slab row
 constexpr int kFitBatch = 64;  // contexts per launch
 constexpr int kNB = 32;        // Cholesky panel width
 
-int32_t g_fit_hip = 0;
-
-kvx_status fit_hip_fail(hipError_t e) {
-  g_fit_hip = static_cast<int32_t>(e);
-  return e == hipErrorOutOfMemory ? KVX_ENOMEM : KVX_EHIP;
-}
+kvx_status fit_hip_fail(hipError_t e) { return hip_status(e); }
 
 #define FIT_HIP(x)                                \
   do {                                            \

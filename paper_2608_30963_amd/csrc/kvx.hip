@@ -21,10 +21,7 @@ namespace {
 
 thread_local int32_t g_last_hip = 0;
 
-kvx_status hip_fail(hipError_t e) {
-  g_last_hip = static_cast<int32_t>(e);
-  return e == hipErrorOutOfMemory ? KVX_ENOMEM : KVX_EHIP;
-}
+kvx_status hip_fail(hipError_t e) { return kvx::hip_status(e); }
 
 #define KVX_HIP(x)                          \
   do {                                      \
@@ -35,6 +32,12 @@ kvx_status hip_fail(hipError_t e) {
 enum Kernel { kTiled = 0, kFused = 1 };
 
 }  // namespace
+
+kvx_status kvx::hip_status(hipError_t e) {
+  if (e == hipSuccess) return KVX_OK;
+  g_last_hip = static_cast<int32_t>(e);
+  return e == hipErrorOutOfMemory ? KVX_ENOMEM : KVX_EHIP;
+}
 
 struct kvx_plan {
   int device = 0;

@@ -1,7 +1,8 @@
 """Python binding of ``libkvx.so`` (argument marshalling only).
 
-The entry points carry the C names -- ``kvx_plan_create``, ``kvx_translate``,
-``kvx_plan_destroy`` (include/kvx.h) and ``kvx_fit_create``,
+The entry points carry the C names -- ``kvx_plan_create``,
+``kvx_plan_create_factored``, ``kvx_translate``, ``kvx_plan_destroy``
+(include/kvx.h) and ``kvx_fit_create``,
 ``kvx_fit_accumulate``, ``kvx_fit_solve``, ``kvx_fit_reset``,
 ``kvx_fit_destroy`` (include/kvx_fit.h) -- and take torch tensors for device
 buffers (torch provides device memory and streams; it computes nothing here).
@@ -24,9 +25,11 @@ LIB_PATH = os.path.join(HERE, "libkvx.so")
 KVX_OK, KVX_EINVAL, KVX_ESHAPE, KVX_EUNSUPPORTED, KVX_ENOMEM, KVX_EHIP, KVX_EDATA = range(7)
 KVX_F32, KVX_BF16 = 0, 1
 KVX_PREC_BF16X2, KVX_PREC_BF16, KVX_PREC_F16 = 0, 1, 2
+KVX_FACTORS_LOWRANK, KVX_FACTORS_MIXTURE = 1, 2
 
 # Exported C symbols, as declared in include/kvx.h and include/kvx_fit.h.
-SYMBOLS = ("kvx_plan_create", "kvx_translate", "kvx_plan_destroy", "kvx_status_string",
+SYMBOLS = ("kvx_plan_create", "kvx_plan_create_factored", "kvx_translate", "kvx_plan_destroy",
+           "kvx_status_string",
            "kvx_last_hip_error", "kvx_plan_query", "kvx_fit_create", "kvx_fit_accumulate",
            "kvx_fit_solve", "kvx_fit_reset", "kvx_fit_rows", "kvx_fit_query",
            "kvx_fit_destroy")
@@ -48,6 +51,13 @@ class PlanDesc(C.Structure):
                 ("layer_map", C.c_void_p), ("dtype", C.c_int32),
                 ("w_k", C.c_void_p), ("w_v", C.c_void_p),
                 ("b_k", C.c_void_p), ("b_v", C.c_void_p), ("precision", C.c_int32)]
+
+
+class Factors(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("rank", C.c_int32), ("u_k", C.c_void_p),
+                ("u_v", C.c_void_p), ("v_k", C.c_void_p), ("v_v", C.c_void_p),
+                ("n_mix", C.c_int32), ("alpha", C.c_void_p), ("w_k", C.c_void_p),
+                ("w_v", C.c_void_p), ("b_k", C.c_void_p), ("b_v", C.c_void_p)]
 
 
 class IO(C.Structure):
@@ -99,6 +109,9 @@ def load(path: str = LIB_PATH):
     lib = C.CDLL(path)
     lib.kvx_plan_create.argtypes = [C.POINTER(PlanDesc), C.POINTER(C.c_void_p)]
     lib.kvx_plan_create.restype = C.c_int
+    lib.kvx_plan_create_factored.argtypes = [C.POINTER(PlanDesc), C.POINTER(Factors),
+                                             C.POINTER(C.c_void_p)]
+    lib.kvx_plan_create_factored.restype = C.c_int
     lib.kvx_translate.argtypes = [C.c_void_p, C.POINTER(IO), C.c_void_p]
     lib.kvx_translate.restype = C.c_int
     lib.kvx_plan_destroy.argtypes = [C.c_void_p]
@@ -182,6 +195,43 @@ def kvx_plan_create(src, tgt, mix: int, layer_map: Sequence[int], dtype: int, w_
     return h.value
 
 
+def kvx_plan_create_factored(src, tgt, mix: int, layer_map: Sequence[int], dtype: int,
+                             lowrank=None, mixture=None, b_k=None, b_v=None,
+                             precision: int = KVX_PREC_BF16X2, src_inv_freq=None,
+                             tgt_inv_freq=None) -> int:
+    """Create a plan from translator factors; returns the handle.
+    ``lowrank=(u_k, v_k, u_v, v_v)`` (device [Lt][dout][r], [Lt][r][din];
+    ``b_k``/``b_v`` give its bias) or ``mixture=(alpha, w_k, w_v, b_k, b_v)``
+    (host alpha [K]; device [K][Lt][dout][din] and fp32 [K][Lt][dout] or
+    None)."""
+    lib = load()
+    keep = []
+    lm = _host_array([int(x) for x in layer_map], C.c_int32)
+    keep.append(lm)
+    f = Factors()
+    if lowrank is not None:
+        u_k, v_k, u_v, v_v = lowrank
+        f.kind = KVX_FACTORS_LOWRANK
+        f.rank = int(u_k.shape[-1]) if hasattr(u_k, "shape") else 0
+        f.u_k, f.v_k, f.u_v, f.v_v = _ptr(u_k), _ptr(v_k), _ptr(u_v), _ptr(v_v)
+    elif mixture is not None:
+        alpha, w_k, w_v, mb_k, mb_v = mixture
+        al = _host_array([float(x) for x in alpha], C.c_double)
+        keep.append(al)
+        f.kind = KVX_FACTORS_MIXTURE
+        f.n_mix = len(alpha)
+        f.alpha = C.cast(al, C.c_void_p).value
+        f.w_k, f.w_v, f.b_k, f.b_v = _ptr(w_k), _ptr(w_v), _ptr(mb_k), _ptr(mb_v)
+    desc = PlanDesc(_model(src, src_inv_freq, keep), _model(tgt, tgt_inv_freq, keep),
+                    int(mix), C.cast(lm, C.c_void_p).value, int(dtype), None, None,
+                    _ptr(b_k), _ptr(b_v), int(precision))
+    h = C.c_void_p()
+    st = lib.kvx_plan_create_factored(C.byref(desc), C.byref(f), C.byref(h))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_plan_create_factored")
+    return h.value
+
+
 def make_io(batch: int, src_tokens: int, src_k, src_v, tgt_k, tgt_v, tgt_capacity: int,
             tgt_tokens=None, row_ptr=None, col_idx=None, weight=None,
             src_stride=(0, 0, 0, 0), tgt_stride=(0, 0, 0, 0), block_table=None,
@@ -236,12 +286,21 @@ def kvx_plan_query(plan: int) -> PlanInfo:
 class Translator:
     """RAII wrapper around a plan, for the tests and the benchmark."""
 
-    def __init__(self, src, tgt, mix, layer_map, dtype, w_k, w_v, b_k=None, b_v=None,
-                 precision=KVX_PREC_BF16X2, src_inv_freq=None, tgt_inv_freq=None):
+    def __init__(self, src, tgt, mix, layer_map, dtype, w_k=None, w_v=None, b_k=None,
+                 b_v=None, precision=KVX_PREC_BF16X2, src_inv_freq=None, tgt_inv_freq=None,
+                 lowrank=None, mixture=None):
+        """Dense translator from ``w_k``/``w_v``, or a composed one from
+        ``lowrank`` / ``mixture`` (see kvx_plan_create_factored)."""
         self.src, self.tgt, self.mix = src, tgt, mix
         self.dtype = dtype
-        self.plan = kvx_plan_create(src, tgt, mix, layer_map, dtype, w_k, w_v, b_k, b_v,
-                                    precision, src_inv_freq, tgt_inv_freq)
+        self.plan = None
+        if lowrank is not None or mixture is not None:
+            self.plan = kvx_plan_create_factored(src, tgt, mix, layer_map, dtype, lowrank,
+                                                 mixture, b_k, b_v, precision, src_inv_freq,
+                                                 tgt_inv_freq)
+        else:
+            self.plan = kvx_plan_create(src, tgt, mix, layer_map, dtype, w_k, w_v, b_k, b_v,
+                                        precision, src_inv_freq, tgt_inv_freq)
 
     def info(self) -> PlanInfo:
         return kvx_plan_query(self.plan)

@@ -355,6 +355,46 @@ def draw_native_target(spec: Spec, which: int, tgt_tokens) -> np.ndarray:
     return to_storage(out, spec.dtype)
 
 
+def draw_lowrank(spec: Spec, rank: int):
+    """Low-rank translator factors (u_k, v_k, u_v, v_v) in the storage dtype:
+    U [Lt, out, r] ~ N(0, 1/r), V [Lt, r, in] ~ N(0, 1/in), so that U V z has
+    the scale of the dense draw.  Streams (seed, cfg, 11 + which, l, 0 | 1)."""
+    out = []
+    for which in (0, 1):
+        u = np.empty((spec.tgt.n_layers, spec.d_out, rank), dtype=np.float32)
+        v = np.empty((spec.tgt.n_layers, rank, spec.d_in), dtype=np.float32)
+        for l in range(spec.tgt.n_layers):
+            u[l] = _rng(spec, 11 + which, l, 0).standard_normal(
+                (spec.d_out, rank), dtype=np.float32) * np.float32(1.0 / np.sqrt(rank))
+            v[l] = _rng(spec, 11 + which, l, 1).standard_normal(
+                (rank, spec.d_in), dtype=np.float32) * np.float32(1.0 / np.sqrt(spec.d_in))
+        out += [to_storage(u, spec.dtype), to_storage(v, spec.dtype)]
+    return tuple(out)
+
+
+def draw_mixture(spec: Spec, n_mix: int, with_bias: bool = True):
+    """A mixture of ``n_mix`` translators: alpha [K] float64 ~ Dirichlet(1)
+    (stream 15), members w_k, w_v [K, Lt, out, in] ~ N(0, 1/in) in the
+    storage dtype (streams 13 + which, k, l) and biases b_k, b_v fp32
+    [K, Lt, out] ~ N(0, bias_std^2) (streams 17 + which, k, l) or None.
+    Returns (alpha, w_k, w_v, b_k, b_v)."""
+    alpha = _rng(spec, 15).dirichlet(np.ones(n_mix))
+    std = np.float32(1.0 / np.sqrt(spec.d_in))
+    ws, bs = [], []
+    for which in (0, 1):
+        w = np.empty((n_mix, spec.tgt.n_layers, spec.d_out, spec.d_in), dtype=np.float32)
+        b = np.empty((n_mix, spec.tgt.n_layers, spec.d_out), dtype=np.float32)
+        for k in range(n_mix):
+            for l in range(spec.tgt.n_layers):
+                w[k, l] = _rng(spec, 13 + which, k, l).standard_normal(
+                    (spec.d_out, spec.d_in), dtype=np.float32) * std
+                b[k, l] = _rng(spec, 17 + which, k, l).standard_normal(
+                    spec.d_out, dtype=np.float32) * np.float32(spec.bias_std)
+        ws.append(to_storage(w, spec.dtype))
+        bs.append(b if with_bias else None)
+    return alpha, ws[0], ws[1], bs[0], bs[1]
+
+
 def tiny_spec(**kw) -> Spec:
     """A small custom problem for property tests; every field overridable."""
     base = dict(cfg_id=100, name="tiny", src=ModelShape(3, 2, 8, 1.0e4),

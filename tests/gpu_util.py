@@ -43,7 +43,11 @@ def dev_to_f64(t, dtype: str) -> np.ndarray:
 class DevProblem:
     """Device copies of a problem's arrays plus a plan."""
 
-    def __init__(self, prob: S.Problem, precision=kvx.KVX_PREC_BF16X2, cap=None, fill=None):
+    def __init__(self, prob: S.Problem, precision=kvx.KVX_PREC_BF16X2, cap=None, fill=None,
+                 lowrank=None, mixture=None):
+        """``lowrank=(u_k, v_k, u_v, v_v)`` or ``mixture=(alpha, w_k, w_v, b_k,
+        b_v)`` (host arrays in the storage dtype, biases fp32) build the plan
+        from translator factors instead of the problem's dense weights."""
         T = torch()
         spec = prob.spec
         self.prob = prob
@@ -59,8 +63,19 @@ class DevProblem:
         self.row_ptr = np_to_dev(prob.row_ptr, S.F32) if prob.row_ptr is not None else None
         self.col_idx = np_to_dev(prob.col_idx, S.F32) if prob.col_idx is not None else None
         self.weight = np_to_dev(prob.weight, S.F32) if prob.weight is not None else None
+        self.factors = None
+        if lowrank is not None:
+            self.factors = tuple(np_to_dev(a, dt) for a in lowrank)
+            kw = {"lowrank": self.factors}
+        elif mixture is not None:
+            alpha, mw_k, mw_v, mb_k, mb_v = mixture
+            self.factors = (np_to_dev(mw_k, dt), np_to_dev(mw_v, dt), np_to_dev(mb_k, S.F32),
+                            np_to_dev(mb_v, S.F32))
+            kw = {"mixture": (list(alpha),) + self.factors}
+        else:
+            kw = {"w_k": self.w_k, "w_v": self.w_v}
         self.tr = kvx.Translator(spec.src, spec.tgt, spec.mix, spec.layer_map, self.kdtype,
-                                 self.w_k, self.w_v, self.b_k, self.b_v, precision)
+                                 b_k=self.b_k, b_v=self.b_v, precision=precision, **kw)
         self.cap = prob.tgt_capacity if cap is None else cap
         shape = (spec.tgt.n_layers, spec.batch, spec.tgt.n_kv_heads, self.cap,
                  spec.tgt.head_dim)

@@ -154,3 +154,35 @@ def test_fit_calls_reject_null():
     info = kvx.FitInfo()
     assert lib.kvx_fit_query(None, C.byref(info)) == kvx.KVX_EINVAL
     kvx.kvx_fit_destroy(None)
+
+
+def _factored(desc, f):
+    h = C.c_void_p(12345)
+    st = kvx.load().kvx_plan_create_factored(C.byref(desc), C.byref(f), C.byref(h))
+    return st, h.value
+
+
+def test_plan_create_factored_rejects_bad_arguments():
+    """Every rejection here happens on the host, before any device work."""
+    lib = kvx.load()
+    d, keep = _desc(w_k=None, w_v=None)
+    lr = dict(kind=kvx.KVX_FACTORS_LOWRANK, rank=4, u_k=0x10, u_v=0x20, v_k=0x30, v_v=0x40)
+    assert lib.kvx_plan_create_factored(None, None, None) == kvx.KVX_EINVAL
+    assert lib.kvx_plan_create_factored(C.byref(d), None, None) == kvx.KVX_EINVAL
+    f = kvx.Factors(**lr)
+    assert lib.kvx_plan_create_factored(C.byref(d), C.byref(f), None) == kvx.KVX_EINVAL
+    for kw in ({"kind": 0}, {"kind": 3}, {"rank": 0}, {"u_k": None}, {"v_v": None}):
+        st, h = _factored(d, kvx.Factors(**{**lr, **kw}))
+        assert st == kvx.KVX_EINVAL and h is None, kw
+    for dkw in ({"mix": 0}, {"dtype": 7}, {"precision": 9}, {"layer_map": None}):
+        dd, keep2 = _desc(w_k=None, w_v=None, **dkw)
+        assert _factored(dd, kvx.Factors(**lr))[0] == kvx.KVX_EINVAL, dkw
+    alpha = (C.c_double * 40)(*([0.5] * 40))
+    mx = dict(kind=kvx.KVX_FACTORS_MIXTURE, n_mix=2, alpha=C.cast(alpha, C.c_void_p).value,
+              w_k=0x10, w_v=0x20)
+    for kw, status in (({"n_mix": 0}, kvx.KVX_EINVAL), ({"alpha": None}, kvx.KVX_EINVAL),
+                       ({"w_v": None}, kvx.KVX_EINVAL), ({"n_mix": 33}, kvx.KVX_EUNSUPPORTED)):
+        st, h = _factored(d, kvx.Factors(**{**mx, **kw}))
+        assert st == status and h is None, kw
+    alpha[1] = float("nan")
+    assert _factored(d, kvx.Factors(**mx))[0] == kvx.KVX_EINVAL
