@@ -257,13 +257,18 @@ __device__ __forceinline__ void load_blocks(const FusedArgs& a, const Tile& Tc, 
 }
 
 // Staging layout of a finished tile.  Producer thread `it` stores the
-// 16-byte pieces (row it / 32 + 8 j, staged column 8 * (it % 32)), j < 16;
-// piece j lives in the A-buffer slot that the same thread fills in its
-// transform (plane j / 8, unit (j % 8) / 2, half j % 2).  A producer
-// therefore reads all of its staged pieces before its next transform
-// overwrites them, without any other thread touching them in between, and
-// the stores can run in the step after the staging.  Staged column
-// w*64 + p*32 + e holds feature c_p + e of pair block 4*nt + w.
+// 16-byte pieces (row r = it / 32 + 8 j, staged column group
+// (it % 32) ^ stage_swz(r)), j < 16; piece j lives in the A-buffer slot that
+// the same thread fills in its transform (plane j / 8, unit (j % 8) / 2,
+// half j % 2).  A producer therefore reads all of its staged pieces before
+// its next transform overwrites them, without any other thread touching them
+// in between, and the stores can run in the step after the staging.  Staged
+// column w*64 + p*32 + e holds feature c_p + e of pair block 4*nt + w.
+// The swizzle spreads the 32 rows that one staging write of a consumer wave
+// covers over the LDS banks (four times fewer bank conflicts than the plain
+// layout); a store still covers whole rows, so its coalescing is unchanged.
+__device__ __forceinline__ int stage_swz(int row) { return row & 24; }
+
 __device__ __forceinline__ int stage_slot(int it, int j) {
   return (j / 8) * kPlane + (it / 8 + 32 * ((j % 8) / 2)) * kLDA + 64 * (j % 2) + 8 * (it % 8);
 }
@@ -280,7 +285,7 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
   for (int i = 0; i < kRowsPerThread; ++i) {
     const int pc = it + 256 * i;
     const int r = pc / (kNT / 8);
-    const int sc8 = pc % (kNT / 8);   // staged column / 8
+    const int sc8 = (pc % (kNT / 8)) ^ stage_swz(r);  // staged column / 8
     const int w = sc8 / 8;            // owning consumer wave (pair block)
     const int pbw = Tc.nt * 4 + w;
     const int t = Tc.t0 + r;
@@ -800,8 +805,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         const bf16x2 p10 = {static_cast<__bf16>(u1[0]), static_cast<__bf16>(u1[1])};
         const bf16x2 p11 = {static_cast<__bf16>(u1[2]), static_cast<__bf16>(u1[3])};
         // staged columns cw*64 + p*32 + 8*g4 + fq .. +3 of this row (p = 1:
-        // piece owner it + 4, whose slot is 32 elements further)
-        bf16_t* sp = st + stage_slot((row % 8) * 32 + cw * 8 + g4, row / 8) + fq;
+        // piece owner it + 4 -- the swizzle leaves bit 2 alone -- whose slot
+        // is 32 elements further)
+        bf16_t* sp = st + stage_slot((row % 8) * 32 + ((cw * 8 + g4) ^ stage_swz(row)), row / 8) + fq;
         *reinterpret_cast<uint2*>(sp) =
             make_uint2(__builtin_bit_cast(uint32_t, p00), __builtin_bit_cast(uint32_t, p01));
         *reinterpret_cast<uint2*>(sp + 32) =

@@ -106,6 +106,10 @@ def load(path: str = LIB_PATH):
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with "
                            "`python -m paper_2608_30963_amd.build` (no fallback exists)")
+    # torch provides the device memory and streams; its HIP runtime must be
+    # the process's only one, so it is loaded before the library binds to
+    # whichever runtime is already present
+    import torch  # noqa: F401
     lib = C.CDLL(path)
     lib.kvx_plan_create.argtypes = [C.POINTER(PlanDesc), C.POINTER(C.c_void_p)]
     lib.kvx_plan_create.restype = C.c_int
