@@ -138,7 +138,9 @@ def main():
     ap.add_argument("--tokens", type=int, default=None, help="override source tokens")
     ap.add_argument("--batch", type=int, default=None, help="override contexts per call")
     ap.add_argument("--sets", type=int, default=3, help="rotating buffer sets")
-    ap.add_argument("--precision", choices=["bf16x2", "bf16", "f16"], default="bf16x2")
+    ap.add_argument("--precision", choices=["bf16x2", "bf16", "f16", "bf16x2o"], default="bf16x2",
+                    help="operand precision; bf16x2o splits only the k-steps holding the "
+                         "workload's outlier channels")
     ap.add_argument("--paged", type=int, default=0, metavar="BLOCK",
                     help="write a paged target cache with BLOCK tokens per block through a "
                          "shuffled block table (0 = contiguous target layout)")
@@ -186,10 +188,13 @@ def main():
 
     kd = kvx.KVX_BF16 if spec.dtype == "bf16" else kvx.KVX_F32
     prec = {"bf16x2": kvx.KVX_PREC_BF16X2, "bf16": kvx.KVX_PREC_BF16,
-            "f16": kvx.KVX_PREC_F16}[args.precision]
+            "f16": kvx.KVX_PREC_F16, "bf16x2o": kvx.KVX_PREC_BF16X2_OUTLIER}[args.precision]
     w_k, w_v = dev(prob.w_k), dev(prob.w_v)
+    marks = {}
+    if prec == kvx.KVX_PREC_BF16X2_OUTLIER:
+        marks = {"outlier_k": S.outlier_channels(spec, 0), "outlier_v": S.outlier_channels(spec, 1)}
     tr = kvx.Translator(spec.src, spec.tgt, spec.mix, spec.layer_map, kd, w_k, w_v,
-                        dev(prob.b_k), dev(prob.b_v), prec)
+                        dev(prob.b_k), dev(prob.b_v), prec, **marks)
     del w_k, w_v
     info = tr.info()
     ident = prob.row_ptr is None

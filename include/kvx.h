@@ -61,8 +61,22 @@ typedef enum { KVX_F32 = 0, KVX_BF16 = 1 } kvx_dtype;
  *                   overflows and makes the affected outputs non-finite;
  *                   kvx_plan_create returns KVX_EUNSUPPORTED if a weight
  *                   exceeds the fp16 range.
+ *  KVX_PREC_BF16X2_OUTLIER: mixed precision by channel, in the manner of
+ *                   LLM.int8() (Dettmers et al., 2022), which keeps outlier
+ *                   features at higher precision: the computed operands of
+ *                   the 16-feature k-steps that hold a source channel marked
+ *                   in kvx_plan_desc.outlier_k / outlier_v are split as in
+ *                   BF16X2, all others are rounded once as in BF16.  K's
+ *                   de-rotation mixes the two members of a RoPE pair, so a
+ *                   marked K channel also marks its partner (d + Ds/2 mod Ds).
+ *                   With every channel marked it is BF16X2, with none BF16.
  * Accumulation is fp32 in every mode. */
-typedef enum { KVX_PREC_BF16X2 = 0, KVX_PREC_BF16 = 1, KVX_PREC_F16 = 2 } kvx_precision;
+typedef enum {
+  KVX_PREC_BF16X2 = 0,
+  KVX_PREC_BF16 = 1,
+  KVX_PREC_F16 = 2,
+  KVX_PREC_BF16X2_OUTLIER = 3
+} kvx_precision;
 
 /* One side of the translation (a model's KV-cache geometry). */
 typedef struct {
@@ -88,6 +102,12 @@ typedef struct {
   const float* b_k;          /* device fp32 [Lt][Ht*Dt], or NULL for zero bias */
   const float* b_v;
   int32_t precision;         /* kvx_precision */
+  /* Outlier channels of the source cache, read by KVX_PREC_BF16X2_OUTLIER
+   * only (ignored otherwise): host [src.n_layers][src.n_kv_heads][src.head_dim],
+   * nonzero marks channel (layer, head, dim) of source K (outlier_k) or V
+   * (outlier_v); NULL marks none.  Copied into the plan's split table. */
+  const uint8_t* outlier_k;
+  const uint8_t* outlier_v;
 } kvx_plan_desc;
 
 /* One translation call.  Strides are in elements, for (layer, batch, head,
@@ -199,6 +219,11 @@ typedef struct {
   int32_t threads;       /* threads per workgroup */
   int32_t precision;     /* kvx_precision of the plan */
   int64_t weight_bytes;  /* device bytes held by the plan */
+  /* KVX_PREC_BF16X2_OUTLIER on the fused kernel: of the `ksteps` 16-feature
+   * k-steps of all target layers' K and V contractions, `split_ksteps` take
+   * the split operand (when the operand is computed).  Both 0 otherwise. */
+  int64_t split_ksteps;
+  int64_t ksteps;
 } kvx_plan_info;
 
 kvx_status kvx_plan_query(const kvx_plan* plan, kvx_plan_info* info);

@@ -77,6 +77,10 @@ struct FusedArgs {
   const bf16_t* zsink;      // kSinkBytes of zeros: source of lanes without data
   bf16_t* trash;            // kSinkBytes never read: target of lanes without a row
   Paging pg;                // optional paged target layout
+  // split table of precision BF16X2_OUTLIER: bit ks of entry
+  // (l * 2 + kv) * (din / 128) + c marks k-step ks of chunk c as split;
+  // NULL: every k-step of a computed operand is split
+  const uint8_t* split_mask;
   BatchArgs ba;
 };
 
@@ -830,6 +834,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     if (c < nch) {
       // ---------------- chunk step ----------------
       const bool computed = T.kv == 0 || !IDENT;
+      // k-steps of this chunk that take the split operand (a uniform load)
+      const int kmask =
+          PREC == kBF16X2 && a.split_mask ? a.split_mask[(T.l * 2 + T.kv) * nch + c] : 0xFF;
       // weights four k-steps ahead (k-steps 4..7 of this chunk, then 0..3 of
       // the next chunk, possibly of the next tile): a ring slot is reloaded
       // as soon as the MFMAs of its k-step have issued
@@ -893,14 +900,15 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         frag(hi, 0, za);
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) {
-          if (split) frag(lo, ks, zb);
+          const bool split_ks = split && ((kmask >> ks) & 1);
+          if (split_ks) frag(lo, ks, zb);
           __builtin_amdgcn_sched_barrier(0);
           if (ks == 0 && c == 0) mfma8(ks, za, true);
           else mfma8(ks, za, false);
           __builtin_amdgcn_sched_barrier(0);
           if (ks + 1 < 8) frag(hi, ks + 1, za);
           __builtin_amdgcn_sched_barrier(0);
-          if (split) mfma8(ks, zb, false);
+          if (split_ks) mfma8(ks, zb, false);
           reload(ks);
           __builtin_amdgcn_sched_barrier(0);
         }

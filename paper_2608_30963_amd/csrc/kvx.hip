@@ -61,6 +61,8 @@ struct kvx_plan {
   // every global access of the kernel is unconditional
   void* zsink = nullptr;
   void* trash = nullptr;
+  uint8_t* split_mask = nullptr; // precision BF16X2_OUTLIER: [Lt][2][din/128]
+  int64_t split_ksteps = 0, ksteps = 0;
   void* block = nullptr;         // single allocation backing all of the above
 };
 
@@ -131,7 +133,7 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   if (!valid_model(d->src) || !valid_model(d->tgt) || d->mix < 1) return KVX_EINVAL;
   if (d->dtype != KVX_F32 && d->dtype != KVX_BF16) return KVX_EINVAL;
   if (d->precision != KVX_PREC_BF16X2 && d->precision != KVX_PREC_BF16 &&
-      d->precision != KVX_PREC_F16)
+      d->precision != KVX_PREC_F16 && d->precision != KVX_PREC_BF16X2_OUTLIER)
     return KVX_EINVAL;
   if (d->src.head_dim % 2 || d->tgt.head_dim % 2) return KVX_EUNSUPPORTED;
   const int64_t lt = d->tgt.n_layers;
@@ -182,8 +184,12 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   size_t off_b0 = off_h1 + align256(hbytes);
   size_t off_b1 = off_b0 + align256(bbytes), off_m = off_b1 + align256(bbytes);
   size_t off_fs = off_m + align256(mbytes), off_ft = off_fs + align256(fsb);
+  const bool want_mask = p->kernel == kFused && d->precision == KVX_PREC_BF16X2_OUTLIER;
+  const int64_t nch = din64 / 128;
+  const size_t smb = want_mask ? size_t(lt) * 2 * nch : 0;
   size_t off_sink = off_ft + align256(ftb);
-  size_t total = off_sink + 2 * kSinkBytes;
+  size_t off_sm = off_sink + 2 * kSinkBytes;
+  size_t total = off_sm + align256(smb);
   e = hipMalloc(&p->block, total);
   if (e != hipSuccess) return fail(hip_fail(e));
   p->bytes = static_cast<int64_t>(total);
@@ -201,6 +207,7 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   p->ft = reinterpret_cast<double*>(base + off_ft);
   p->zsink = base + off_sink;
   p->trash = base + off_sink + kSinkBytes;
+  if (want_mask) p->split_mask = reinterpret_cast<uint8_t*>(base + off_sm);
   e = hipMemset(p->zsink, 0, kSinkBytes);
   if (e != hipSuccess) return fail(hip_fail(e));
 
@@ -267,6 +274,29 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   if (e != hipSuccess) return fail(hip_fail(e));
   e = hipMemcpy(p->ft, ftv.data(), ftb, hipMemcpyHostToDevice);
   if (e != hipSuccess) return fail(hip_fail(e));
+  if (want_mask) {
+    // Bit ks of entry (l, kv, c): k-step ks of chunk c holds a marked channel
+    // (for K, also a channel whose RoPE partner is marked).
+    const int hs = d->src.n_kv_heads, ds = d->src.head_dim;
+    std::vector<uint8_t> sm(smb, 0);
+    const uint8_t* marks[2] = {d->outlier_k, d->outlier_v};
+    for (int64_t l = 0; l < lt; ++l)
+      for (int kv = 0; kv < 2; ++kv)
+        for (int64_t k = 0; k < din64; ++k) {
+          if (!marks[kv]) break;
+          const int64_t f = fused_feature_of_slot(k, ds);
+          const int64_t j = f / (int64_t(hs) * ds), h = (f / ds) % hs, dd = f % ds;
+          const int64_t ls = d->layer_map[l * d->mix + j];
+          const uint8_t* row = marks[kv] + (ls * hs + h) * ds;
+          const bool hit = row[dd] != 0 || (kv == 0 && row[(dd + ds / 2) % ds] != 0);
+          if (hit) sm[(l * 2 + kv) * nch + k / 128] |= uint8_t(1u << ((k % 128) / 16));
+        }
+    for (uint8_t b : sm)
+      for (int i = 0; i < 8; ++i) p->split_ksteps += (b >> i) & 1;
+    p->ksteps = int64_t(smb) * 8;
+    e = hipMemcpy(p->split_mask, sm.data(), smb, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(hip_fail(e));
+  }
   e = hipDeviceSynchronize();
   if (e != hipSuccess) return fail(hip_fail(e));
   *out = p;
@@ -287,6 +317,8 @@ kvx_status kvx_plan_query(const kvx_plan* p, kvx_plan_info* info) {
   info->threads = p->kernel == kFused ? kThreads : 256;
   info->precision = p->precision;
   info->weight_bytes = p->bytes;
+  info->split_ksteps = p->split_ksteps;
+  info->ksteps = p->ksteps;
   return KVX_OK;
 }
 
@@ -483,6 +515,7 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       a.n_tiles = (p->dout / 64 + 3) / 4;
       a.row_tiles = tiles;
       a.pg = pg;
+      a.split_mask = p->split_mask;
       a.ba = ba;
       const int64_t total = int64_t(tiles) * a.n_tiles * 2 * Lt;
       if (total > INT32_MAX) return KVX_ESHAPE;

@@ -24,7 +24,7 @@ LIB_PATH = os.path.join(HERE, "libkvx.so")
 
 KVX_OK, KVX_EINVAL, KVX_ESHAPE, KVX_EUNSUPPORTED, KVX_ENOMEM, KVX_EHIP, KVX_EDATA = range(7)
 KVX_F32, KVX_BF16 = 0, 1
-KVX_PREC_BF16X2, KVX_PREC_BF16, KVX_PREC_F16 = 0, 1, 2
+KVX_PREC_BF16X2, KVX_PREC_BF16, KVX_PREC_F16, KVX_PREC_BF16X2_OUTLIER = 0, 1, 2, 3
 KVX_FACTORS_LOWRANK, KVX_FACTORS_MIXTURE = 1, 2
 
 # Exported C symbols, as declared in include/kvx.h and include/kvx_fit.h.
@@ -50,7 +50,8 @@ class PlanDesc(C.Structure):
     _fields_ = [("src", Model), ("tgt", Model), ("mix", C.c_int32),
                 ("layer_map", C.c_void_p), ("dtype", C.c_int32),
                 ("w_k", C.c_void_p), ("w_v", C.c_void_p),
-                ("b_k", C.c_void_p), ("b_v", C.c_void_p), ("precision", C.c_int32)]
+                ("b_k", C.c_void_p), ("b_v", C.c_void_p), ("precision", C.c_int32),
+                ("outlier_k", C.c_void_p), ("outlier_v", C.c_void_p)]
 
 
 class Factors(C.Structure):
@@ -92,7 +93,8 @@ class FitInfo(C.Structure):
 
 class PlanInfo(C.Structure):
     _fields_ = [("kernel", C.c_int32), ("tile_rows", C.c_int32), ("tile_cols", C.c_int32),
-                ("threads", C.c_int32), ("precision", C.c_int32), ("weight_bytes", C.c_int64)]
+                ("threads", C.c_int32), ("precision", C.c_int32), ("weight_bytes", C.c_int64),
+                ("split_ksteps", C.c_int64), ("ksteps", C.c_int64)]
 
 
 _lib = None
@@ -180,18 +182,37 @@ def _model(m, inv_freq, keep) -> Model:
                  C.cast(inv, C.c_void_p).value if inv is not None else None)
 
 
+def _marks(arr, src, keep):
+    """Host outlier marks [Ls][Hs][Ds] (any array-like, nonzero = marked) as a
+    uint8 buffer, or None."""
+    if arr is None:
+        return None
+    import numpy as np
+    a = np.ascontiguousarray(np.asarray(arr) != 0, dtype=np.uint8)
+    want = (int(src.n_layers), int(src.n_kv_heads), int(src.head_dim))
+    if a.shape != want:
+        raise ValueError(f"outlier marks have shape {a.shape}, expected {want}")
+    buf = (C.c_uint8 * a.size).from_buffer_copy(a.tobytes())
+    keep.append(buf)
+    return C.cast(buf, C.c_void_p).value
+
+
 def kvx_plan_create(src, tgt, mix: int, layer_map: Sequence[int], dtype: int, w_k, w_v,
                     b_k=None, b_v=None, precision: int = KVX_PREC_BF16X2,
-                    src_inv_freq=None, tgt_inv_freq=None) -> int:
+                    src_inv_freq=None, tgt_inv_freq=None, outlier_k=None,
+                    outlier_v=None) -> int:
     """Create a plan; returns the opaque handle (an int).  ``w_k``/``w_v``/
-    ``b_k``/``b_v`` are device tensors (or raw device pointers)."""
+    ``b_k``/``b_v`` are device tensors (or raw device pointers);
+    ``outlier_k``/``outlier_v`` host marks [Ls][Hs][Ds] for precision
+    KVX_PREC_BF16X2_OUTLIER."""
     lib = load()
     keep = []
     lm = _host_array([int(x) for x in layer_map], C.c_int32)
     keep.append(lm)
     desc = PlanDesc(_model(src, src_inv_freq, keep), _model(tgt, tgt_inv_freq, keep),
                     int(mix), C.cast(lm, C.c_void_p).value, int(dtype), _ptr(w_k), _ptr(w_v),
-                    _ptr(b_k), _ptr(b_v), int(precision))
+                    _ptr(b_k), _ptr(b_v), int(precision), _marks(outlier_k, src, keep),
+                    _marks(outlier_v, src, keep))
     h = C.c_void_p()
     st = lib.kvx_plan_create(C.byref(desc), C.byref(h))
     if st != KVX_OK:
@@ -292,7 +313,7 @@ class Translator:
 
     def __init__(self, src, tgt, mix, layer_map, dtype, w_k=None, w_v=None, b_k=None,
                  b_v=None, precision=KVX_PREC_BF16X2, src_inv_freq=None, tgt_inv_freq=None,
-                 lowrank=None, mixture=None):
+                 lowrank=None, mixture=None, outlier_k=None, outlier_v=None):
         """Dense translator from ``w_k``/``w_v``, or a composed one from
         ``lowrank`` / ``mixture`` (see kvx_plan_create_factored)."""
         self.src, self.tgt, self.mix = src, tgt, mix
@@ -304,7 +325,8 @@ class Translator:
                                                  tgt_inv_freq)
         else:
             self.plan = kvx_plan_create(src, tgt, mix, layer_map, dtype, w_k, w_v, b_k, b_v,
-                                        precision, src_inv_freq, tgt_inv_freq)
+                                        precision, src_inv_freq, tgt_inv_freq, outlier_k,
+                                        outlier_v)
 
     def info(self) -> PlanInfo:
         return kvx_plan_query(self.plan)

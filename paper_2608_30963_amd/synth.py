@@ -295,11 +295,27 @@ def draw_source(spec: Spec, which: int, layers=None) -> np.ndarray:
             out[ls, b] = _rng(spec, which, ls, b).standard_normal(
                 (s.n_kv_heads, spec.src_tokens, s.head_dim), dtype=np.float32)
         if spec.outliers:
-            r = _rng(spec, 2 + which, ls)
+            marks = _outlier_marks(spec, which, ls)
             for h in range(s.n_kv_heads):
-                ch = r.choice(s.head_dim, size=spec.outliers, replace=False)
-                out[ls, :, h, :, ch] *= np.float32(spec.outlier_scale)
+                out[ls, :, h, :, marks[h]] *= np.float32(spec.outlier_scale)
     return out
+
+
+def _outlier_marks(spec: Spec, which: int, ls: int) -> np.ndarray:
+    """Outlier channels of source layer ``ls``: bool [Hs, Ds]."""
+    s = spec.src
+    marks = np.zeros((s.n_kv_heads, s.head_dim), dtype=bool)
+    if spec.outliers:
+        r = _rng(spec, 2 + which, ls)
+        for h in range(s.n_kv_heads):
+            marks[h, r.choice(s.head_dim, size=spec.outliers, replace=False)] = True
+    return marks
+
+
+def outlier_channels(spec: Spec, which: int) -> np.ndarray:
+    """The channels that draw_source scales, K (which=0) or V (which=1):
+    bool [Ls, Hs, Ds] (all False without outliers)."""
+    return np.stack([_outlier_marks(spec, which, ls) for ls in range(spec.src.n_layers)])
 
 
 def draw_weights(spec: Spec, which: int) -> np.ndarray:

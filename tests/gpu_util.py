@@ -44,10 +44,12 @@ class DevProblem:
     """Device copies of a problem's arrays plus a plan."""
 
     def __init__(self, prob: S.Problem, precision=kvx.KVX_PREC_BF16X2, cap=None, fill=None,
-                 lowrank=None, mixture=None):
+                 lowrank=None, mixture=None, outliers=None):
         """``lowrank=(u_k, v_k, u_v, v_v)`` or ``mixture=(alpha, w_k, w_v, b_k,
         b_v)`` (host arrays in the storage dtype, biases fp32) build the plan
-        from translator factors instead of the problem's dense weights."""
+        from translator factors instead of the problem's dense weights;
+        ``outliers=(marks_k, marks_v)`` are the source outlier channels of
+        precision KVX_PREC_BF16X2_OUTLIER."""
         T = torch()
         spec = prob.spec
         self.prob = prob
@@ -74,6 +76,8 @@ class DevProblem:
             kw = {"mixture": (list(alpha),) + self.factors}
         else:
             kw = {"w_k": self.w_k, "w_v": self.w_v}
+        if outliers is not None:
+            kw["outlier_k"], kw["outlier_v"] = outliers
         self.tr = kvx.Translator(spec.src, spec.tgt, spec.mix, spec.layer_map, self.kdtype,
                                  b_k=self.b_k, b_v=self.b_v, precision=precision, **kw)
         self.cap = prob.tgt_capacity if cap is None else cap

@@ -186,3 +186,12 @@ def test_plan_create_factored_rejects_bad_arguments():
         assert st == status and h is None, kw
     alpha[1] = float("nan")
     assert _factored(d, kvx.Factors(**mx))[0] == kvx.KVX_EINVAL
+
+
+def test_outlier_marks_shape_is_checked():
+    src = kvx.ModelShape(2, 2, 8, 1e4)
+    with pytest.raises(ValueError):
+        kvx._marks([[0] * 8] * 2, src, [])
+    keep = []
+    assert kvx._marks(None, src, keep) is None
+    assert kvx._marks([[[1] * 8] * 2] * 2, src, keep) is not None and len(keep) == 1
