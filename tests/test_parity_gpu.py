@@ -80,11 +80,11 @@ def _sample_rows(prob, n_layers_pick, rng):
     return np.array(L), np.array(B), np.array(T)
 
 
-def _sampled(spec, precision=kvx.KVX_PREC_BF16X2, n_layers_pick=3):
+def _sampled(spec, precision=kvx.KVX_PREC_BF16X2, n_layers_pick=3, outliers=None):
     rng = np.random.default_rng(spec.cfg_id)
     prob = S.make_problem(spec)
     print(f"[parity-sampled] {spec.name} T={spec.src_tokens} B={spec.batch}", flush=True)
-    dev = U.DevProblem(prob, precision)
+    dev = U.DevProblem(prob, precision, outliers=outliers)
     dev.run()
     U.torch().cuda.synchronize()
     L, B, T = _sample_rows(prob, n_layers_pick, rng)
@@ -113,6 +113,18 @@ def test_config2_full_size_sampled():
 
 def test_config2_full_size_sampled_f16():
     _sampled(S.config(2), precision=kvx.KVX_PREC_F16)
+
+
+def test_config2_full_size_sampled_outlier_mode():
+    spec = S.config(2)
+    _sampled(spec, precision=kvx.KVX_PREC_BF16X2_OUTLIER,
+             outliers=(S.outlier_channels(spec, 0), S.outlier_channels(spec, 1)))
+
+
+def test_config5_full_size_sampled_outlier_mode():
+    spec = S.config(5)
+    _sampled(spec, precision=kvx.KVX_PREC_BF16X2_OUTLIER, n_layers_pick=2,
+             outliers=(S.outlier_channels(spec, 0), S.outlier_channels(spec, 1)))
 
 
 def test_config3_full_size_sampled():
