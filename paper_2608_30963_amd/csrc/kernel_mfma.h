@@ -900,15 +900,23 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         frag(hi, 0, za);
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) {
+          // unsplit k-steps prefetch the next k-step's fragments into zb
+          // (idle without a split) and move them to za after the group
           const bool split_ks = split && ((kmask >> ks) & 1);
           if (split_ks) frag(lo, ks, zb);
+          else if (ks + 1 < 8) frag(hi, ks + 1, zb);
           __builtin_amdgcn_sched_barrier(0);
           if (ks == 0 && c == 0) mfma8(ks, za, true);
           else mfma8(ks, za, false);
           __builtin_amdgcn_sched_barrier(0);
-          if (ks + 1 < 8) frag(hi, ks + 1, za);
+          if (split_ks && ks + 1 < 8) frag(hi, ks + 1, za);
           __builtin_amdgcn_sched_barrier(0);
-          if (split_ks) mfma8(ks, zb, false);
+          if (split_ks) {
+            mfma8(ks, zb, false);
+          } else if (ks + 1 < 8) {
+#pragma unroll
+            for (int m = 0; m < 4; ++m) za[m] = zb[m];
+          }
           reload(ks);
           __builtin_amdgcn_sched_barrier(0);
         }
