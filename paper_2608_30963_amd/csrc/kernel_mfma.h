@@ -505,6 +505,36 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
 
     float csc[CS_CACHE ? kUnits : 1][8], css[CS_CACHE ? kUnits : 1][8];
 
+    // Span map, contiguous target: second-entry data of the chunk at tpos
+    // (the next one to be transformed), requested at the end of the previous
+    // chunk's transform so that a whole step covers its latency.  (The paged
+    // variant, which holds its block ids as well, reads second entries in
+    // the transform like later ones: the prefetch would spill there.)
+    constexpr bool kPrefetch2 = !IDENT && !PAGED;
+    uint4 yb0[kPrefetch2 ? kUnits : 1], yb1[kPrefetch2 ? kUnits : 1];
+    float ybw[kPrefetch2 ? kUnits : 1];  // its pooling weight (0: no second entry)
+    int ybk[kPrefetch2 ? kUnits : 1];    // and source token
+    auto second_issue = [&](const Raw& R, bool exists) KVX_INLINE {
+      if constexpr (kPrefetch2) {
+        const bf16_t* gp = group_ptr(tpos);
+#pragma unroll
+        for (int u = 0; u < kUnits; ++u) {
+          // unconditional loads from valid addresses: without a second entry
+          // the token, weight and data come from the zero sink
+          const bool two = exists && R.ri.e1[u] - R.ri.e0[u] >= 2;
+          const int32_t* ci = two ? a.col_idx + R.ri.e0[u] + 1
+                                  : reinterpret_cast<const int32_t*>(a.zsink);
+          const float* wi = two ? a.weight + R.ri.e0[u] + 1
+                                : reinterpret_cast<const float*>(a.zsink);
+          ybk[u] = *ci;
+          ybw[u] = *wi;
+          const bf16_t* q = two ? gp + ybk[u] * a.ss.t : a.zsink;
+          yb0[u] = ld_src<STREAM>(q);
+          yb1[u] = ld_src<STREAM>(q + a.ds / 2);
+        }
+      }
+    };
+
     // Transform the chunk at tpos (chunks are transformed in order).
     auto transform = [&](const Raw& R, bf16_t* hi, bf16_t* lo) KVX_INLINE {
       const Tile T = tpos.T;
@@ -564,8 +594,29 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
             z1[i] = w * y1;
           }
         }
-        if (!IDENT) {
-          for (int e = R.ri.e0[u] + 1; e < R.ri.e1[u]; ++e) {
+        if constexpr (kPrefetch2) {
+          // second entry, requested a step earlier (second_issue); zeros and
+          // a zero weight when absent
+          const int k = ybk[u];
+          const float w = ybw[u];
+          float x0[8], x1[8];
+          unpack8(yb0[u], x0);
+          unpack8(yb1[u], x1);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            float v0 = x0[i], v1 = x1[i];
+            if (is_k) {
+              float cs_, sn;
+              rope_cs(f[i], k, cs_, sn);
+              v0 = x0[i] * cs_ + x1[i] * sn;
+              v1 = x1[i] * cs_ - x0[i] * sn;
+            }
+            z0[i] += w * v0;
+            z1[i] += w * v1;
+          }
+        }
+        if constexpr (!IDENT) {
+          for (int e = R.ri.e0[u] + (kPrefetch2 ? 2 : 1); e < R.ri.e1[u]; ++e) {
             const int k = a.col_idx[e];
             const float w = a.weight[e];
             const bf16_t* p = pg.p + k * a.ss.t;
@@ -612,7 +663,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     if constexpr (kDepth == 3) fetch_issue(fetch_addr(nchunks > 2), rC, nchunks > 2);
     {
       const bf16_t* gp = fetch_addr(nchunks > kDepth);
+      second_issue(rA, true);
       transform(rA, lds, lds + kPlane);
+      second_issue(rB, nchunks > 1);
       fetch_issue(gp, rA, nchunks > kDepth);
     }
     lds_barrier();
@@ -681,30 +734,31 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // tpos.ord * spt + tpos.c) during the step before it, from raw set R, and
     // refill R with the chunk kDepth further on.  Called with the sets in turn
     // (chunk mod kDepth), so each set keeps its registers.
-    auto produce = [&](int next, Raw& R) KVX_INLINE {
+    auto produce = [&](int next, Raw& R, const Raw& Rn) KVX_INLINE {
       while (s + 1 < tpos.ord * spt + tpos.c) end_step();  // steps with nothing to transform
       bf16_t* buf = lds + ((s + 1) & 1) * 2 * kPlane;
       const bool more = next + kDepth < nchunks;
       const bf16_t* gp = fetch_addr(more);
       transform(R, buf, buf + kPlane);
+      second_issue(Rn, next + 1 < nchunks);  // Rn: the chunk after this one
       fetch_issue(gp, R, more);
       end_step();
     };
     int next = 1;
     if constexpr (kDepth == 3) {
       for (; next + 2 < nchunks; next += 3) {
-        produce(next, rB);
-        produce(next + 1, rC);
-        produce(next + 2, rA);
+        produce(next, rB, rC);
+        produce(next + 1, rC, rA);
+        produce(next + 2, rA, rB);
       }
-      if (next < nchunks) produce(next, rB);
-      if (next + 1 < nchunks) produce(next + 1, rC);
+      if (next < nchunks) produce(next, rB, rC);
+      if (next + 1 < nchunks) produce(next + 1, rC, rA);
     } else {
       for (; next + 1 < nchunks; next += 2) {
-        produce(next, rB);
-        produce(next + 1, rA);
+        produce(next, rB, rA);
+        produce(next + 1, rA, rB);
       }
-      if (next < nchunks) produce(next, rB);
+      if (next < nchunks) produce(next, rB, rA);
     }
     while (s < nsteps) end_step();
     return;
