@@ -517,17 +517,25 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     auto second_issue = [&](const Raw& R, bool exists) KVX_INLINE {
       if constexpr (kPrefetch2) {
         const bf16_t* gp = group_ptr(tpos);
+        // the second entries' tokens and weights are those of the tile:
+        // (re)read at its first chunk only
+        if (tpos.c == 0) {
+#pragma unroll
+          for (int u = 0; u < kUnits; ++u) {
+            // unconditional loads from valid addresses: without a second
+            // entry the token and weight come from the zero sink
+            const bool two = R.ri.e1[u] - R.ri.e0[u] >= 2;
+            const int32_t* ci = two ? a.col_idx + R.ri.e0[u] + 1
+                                    : reinterpret_cast<const int32_t*>(a.zsink);
+            const float* wi = two ? a.weight + R.ri.e0[u] + 1
+                                  : reinterpret_cast<const float*>(a.zsink);
+            ybk[u] = *ci;
+            ybw[u] = *wi;
+          }
+        }
 #pragma unroll
         for (int u = 0; u < kUnits; ++u) {
-          // unconditional loads from valid addresses: without a second entry
-          // the token, weight and data come from the zero sink
           const bool two = exists && R.ri.e1[u] - R.ri.e0[u] >= 2;
-          const int32_t* ci = two ? a.col_idx + R.ri.e0[u] + 1
-                                  : reinterpret_cast<const int32_t*>(a.zsink);
-          const float* wi = two ? a.weight + R.ri.e0[u] + 1
-                                : reinterpret_cast<const float*>(a.zsink);
-          ybk[u] = *ci;
-          ybw[u] = *wi;
           const bf16_t* q = two ? gp + ybk[u] * a.ss.t : a.zsink;
           yb0[u] = ld_src<STREAM>(q);
           yb1[u] = ld_src<STREAM>(q + a.ds / 2);
