@@ -161,8 +161,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs on one GPU only; the translation shards by "
-              "target layer with no exchange, but multi-GPU runs are not part of it "
+        print("bench.py measures one GPU only: the translation would shard by target "
+              "layer with no exchange, but this benchmark has no multi-GPU mode "
               f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
         sys.exit(2)
 

@@ -38,7 +38,7 @@ typedef enum {
   KVX_OK = 0,
   KVX_EINVAL = 1,       /* NULL or out-of-range argument */
   KVX_ESHAPE = 2,       /* inconsistent dimensions, strides or capacity */
-  KVX_EUNSUPPORTED = 3, /* valid but not supported by this build (e.g. odd head_dim) */
+  KVX_EUNSUPPORTED = 3, /* valid but not supported by this library (e.g. odd head_dim) */
   KVX_ENOMEM = 4,       /* device allocation failed */
   KVX_EHIP = 5,         /* a HIP runtime call failed; see kvx_last_hip_error() */
   KVX_EDATA = 6         /* device CSR contents invalid (validation mode only) */
