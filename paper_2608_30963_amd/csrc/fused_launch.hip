@@ -9,14 +9,23 @@
 namespace kvx {
 namespace {
 
+template <int PREC, bool STREAM, bool PAGED, bool INTER>
+void launch_pspi(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
+  if (identity && ds128)
+    fused_kernel<true, true, PREC, STREAM, PAGED, INTER><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  else if (identity)
+    fused_kernel<true, false, PREC, STREAM, PAGED, INTER><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  else
+    fused_kernel<false, false, PREC, STREAM, PAGED, INTER><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+}
+
+// tile order (interleaved or contiguous ranges) as a template argument
 template <int PREC, bool STREAM, bool PAGED>
 void launch_psp(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
-  if (identity && ds128)
-    fused_kernel<true, true, PREC, STREAM, PAGED><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
-  else if (identity)
-    fused_kernel<true, false, PREC, STREAM, PAGED><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  if (a.interleave)
+    launch_pspi<PREC, STREAM, PAGED, true>(identity, ds128, grid, st, a);
   else
-    fused_kernel<false, false, PREC, STREAM, PAGED><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+    launch_pspi<PREC, STREAM, PAGED, false>(identity, ds128, grid, st, a);
 }
 
 template <int PREC, bool STREAM>

@@ -2,8 +2,9 @@
 //
 // Work unit ("tile"): (target layer l, K|V, 128 target rows of one context,
 // 256 output features).  The kernel is persistent: one workgroup per compute
-// unit walks a contiguous range of tiles (contiguous per XCD, so the weights
-// of a layer stay in that XCD's L2), and its 8 waves run in two roles over
+// unit, each XCD owning a contiguous range of tiles (so the weights of a
+// layer stay in that XCD's L2) that its workgroups take either in contiguous
+// pieces or round-robin (decode_tile), and its 8 waves run in two roles over
 // the concatenated sequence of K-chunks of all its tiles:
 //
 //   producers (waves 0-3)  gather 16-byte pieces of the source rows named by
@@ -74,6 +75,7 @@ struct FusedArgs {
   int32_t n_tiles;          // N tiles per (layer, K|V)
   int32_t row_tiles;        // row tiles of this launch (all contexts)
   int32_t total_tiles;      // row_tiles * n_tiles * 2 * Lt
+  int32_t interleave;       // tile order and assignment (decode_tile); selects the variant
   const bf16_t* zsink;      // kSinkBytes of zeros: source of lanes without data
   bf16_t* trash;            // kSinkBytes never read: target of lanes without a row
   Paging pg;                // optional paged target layout
@@ -94,25 +96,8 @@ constexpr int kMaxHalfDim = 256;    // source head_dim / 2 held in LDS
 
 struct Tile {
   int l, kv, nt, b, t0, tt, rb, rt;
+  int tau;  // linear tile index
 };
-
-// Tile order: layer slowest, then row tile, then N tile, K|V fastest (so a
-// contiguous range mixes K and V tiles and balances their different costs).
-__device__ __forceinline__ Tile decode_tile(const FusedArgs& a, int tau) {
-  Tile T;
-  T.kv = tau % 2;
-  int rest = tau / 2;
-  T.nt = rest % a.n_tiles;
-  rest /= a.n_tiles;
-  const int rt = rest % a.row_tiles;
-  T.rt = rt;
-  T.l = rest / a.row_tiles;
-  T.b = find_context(a.ba, rt);
-  T.t0 = (rt - a.ba.tile_start[T.b]) * kMT;
-  T.tt = a.ba.t_tgt[T.b];
-  T.rb = a.ba.row_base[T.b];
-  return T;
-}
 
 // The launch's context table, copied to LDS at kernel start so the step
 // loop can index it (a dynamic index into the kernel argument would make the
@@ -123,9 +108,52 @@ struct CtxTable {
   int32_t row_base[kMaxBatch];
 };
 
-// The tile after T in the same order, without divisions.
+// Two tile orders, chosen per launch (FusedArgs::interleave):
+//  * contiguous (0): layer slowest, then row tile, then N tile, K|V fastest;
+//    each workgroup walks a contiguous range, so it alternates K and V tiles
+//    (balancing their different costs) and re-reads a row tile's source rows
+//    for its N tiles while they are still in its XCD's L2.
+//  * interleaved (1): layer slowest, then K|V, then row tile, N tile
+//    fastest; each XCD's range is dealt round-robin to its workgroups, which
+//    then run neighbouring tiles at the same time.  They share one layer's
+//    K or V translator in the L2, which pays when a tile's weight slice is
+//    large (long contractions), where contiguous ranges would put several
+//    layers' translators in flight per XCD and re-read them from HBM.
+__device__ __forceinline__ void tile_context(int n_ctx, const CtxTable& cx, Tile& T) {
+  // uniform values: keep them in scalar registers
+  int b = 0;
+  while (b + 1 < n_ctx && __builtin_amdgcn_readfirstlane(cx.tile_start[b + 1]) <= T.rt) ++b;
+  T.b = b;
+  T.t0 = (T.rt - __builtin_amdgcn_readfirstlane(cx.tile_start[b])) * kMT;
+  T.tt = __builtin_amdgcn_readfirstlane(cx.t_tgt[b]);
+  T.rb = __builtin_amdgcn_readfirstlane(cx.row_base[b]);
+}
+__device__ __forceinline__ Tile decode_tile(bool inter, int tau, int n_tiles, int row_tiles,
+                                            int n_ctx, const CtxTable& cx) {
+  Tile T;
+  T.tau = tau;
+  if (inter) {
+    T.nt = tau % n_tiles;
+    int rest = tau / n_tiles;
+    T.rt = rest % row_tiles;
+    rest /= row_tiles;
+    T.kv = rest & 1;
+    T.l = rest >> 1;
+  } else {
+    T.kv = tau & 1;
+    int rest = tau >> 1;
+    T.nt = rest % n_tiles;
+    rest /= n_tiles;
+    T.rt = rest % row_tiles;
+    T.l = rest / row_tiles;
+  }
+  tile_context(n_ctx, cx, T);
+  return T;
+}
+// The next tile of a contiguous range.
 __device__ __forceinline__ void advance_tile(int n_tiles, int row_tiles, int n_ctx,
                                              const CtxTable& cx, Tile& T) {
+  ++T.tau;
   if (T.kv == 0) {
     T.kv = 1;
     return;
@@ -136,13 +164,29 @@ __device__ __forceinline__ void advance_tile(int n_tiles, int row_tiles, int n_c
   if (++T.rt == row_tiles) {
     T.rt = 0;
     ++T.l;
-    T.b = 0;
   }
-  // uniform values: keep them in scalar registers
-  while (T.b + 1 < n_ctx && __builtin_amdgcn_readfirstlane(cx.tile_start[T.b + 1]) <= T.rt) ++T.b;
-  T.t0 = (T.rt - __builtin_amdgcn_readfirstlane(cx.tile_start[T.b])) * kMT;
-  T.tt = __builtin_amdgcn_readfirstlane(cx.t_tgt[T.b]);
-  T.rb = __builtin_amdgcn_readfirstlane(cx.row_base[T.b]);
+  tile_context(n_ctx, cx, T);
+}
+// Interleaved order: advance T by `step` tiles, given step = dr * n_tiles +
+// dn (dn < n_tiles); scalar additions and carries only, no division.
+__device__ __forceinline__ void step_tile(int dn, int dr, int n_tiles, int row_tiles, int n_ctx,
+                                          const CtxTable& cx, Tile& T) {
+  T.tau += dr * n_tiles + dn;
+  T.nt += dn;
+  int r = dr;
+  if (T.nt >= n_tiles) {
+    T.nt -= n_tiles;
+    ++r;
+  }
+  int lk = 2 * T.l + T.kv;
+  T.rt += r;
+  while (T.rt >= row_tiles) {
+    T.rt -= row_tiles;
+    ++lk;
+  }
+  T.kv = lk & 1;
+  T.l = lk >> 1;
+  tile_context(n_ctx, cx, T);
 }
 
 // Workgroup barrier that orders LDS only: waits for this wave's LDS (and
@@ -334,7 +378,7 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
 //
 // STREAM: source rows are read with streaming loads (one N tile, so no tile
 // re-reads them).  PAGED: target rows go through the block table.
-template <bool IDENT, bool CS_CACHE, int PREC, bool STREAM, bool PAGED>
+template <bool IDENT, bool CS_CACHE, int PREC, bool STREAM, bool PAGED, bool INTER>
 __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   // Row stores in the step after the staging (identity alignment), or in the
   // epilogue step itself after a mid-step barrier (span maps: the pooling
@@ -352,14 +396,28 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   __shared__ __attribute__((aligned(16))) float biasl[2][kNT];
   __shared__ CtxTable ctx;
 
+  // Workgroups are dispatched to the 8 XCDs round-robin (block id mod 8).
+  // Each XCD owns a contiguous range of tiles, in proportion to the
+  // workgroups it holds.  Contiguous order: the range is split into one
+  // contiguous piece per workgroup.  Interleaved order: it is dealt
+  // round-robin, workgroup `slot` of the XCD taking tiles xbeg + slot,
+  // xbeg + slot + nq, ...
+  constexpr bool inter = INTER;  // a.interleave, as a template argument
   const int G = gridDim.x;
-  const int wid = xcd_remap(blockIdx.x, G);
-  const int tbeg = static_cast<int>(static_cast<int64_t>(wid) * a.total_tiles / G);
-  const int tend = static_cast<int>(static_cast<int64_t>(wid + 1) * a.total_tiles / G);
+  const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+  const int nq = G / 8 + (xcd < G % 8 ? 1 : 0);          // workgroups on this XCD
+  const int wfirst = xcd * (G / 8) + min(xcd, G % 8);     // and their rank in the grid
+  auto part = [&](int w) KVX_INLINE {
+    return static_cast<int>(static_cast<int64_t>(w) * a.total_tiles / G);
+  };
+  const int xbeg = part(wfirst), xend = part(wfirst + nq);
+  const int tfirst = inter ? xbeg + slot : part(wfirst + slot);
+  const int ntw = inter ? (slot < xend - xbeg ? (xend - xbeg - slot + nq - 1) / nq : 0)
+                        : part(wfirst + slot + 1) - tfirst;  // tiles of this workgroup
   const int nch = a.din / 128;
-  const int spt = nch + 1;                    // steps per tile
-  const int nchunks = (tend - tbeg) * nch;    // chunk steps of this workgroup
-  const int nsteps = (tend - tbeg) * spt;
+  const int spt = nch + 1;            // steps per tile
+  const int nchunks = ntw * nch;      // chunk steps of this workgroup
+  const int nsteps = ntw * spt;
   if (nsteps == 0) return;
   const int tid = threadIdx.x;
   for (int i = tid; i < a.lt * a.mix; i += kThreads) lmap[i] = a.layer_map[i];
@@ -371,7 +429,17 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     }
   }
   const int n_tiles = a.n_tiles, row_tiles = a.row_tiles, n_ctx = a.ba.n;
-  auto next_tile = [&](Tile& T) KVX_INLINE { advance_tile(n_tiles, row_tiles, n_ctx, ctx, T); };
+  auto tile_at = [&](int tau) KVX_INLINE {
+    return decode_tile(inter, tau, n_tiles, row_tiles, n_ctx, ctx);
+  };
+  // the workgroup's next tile (called only while one remains)
+  const int step_dn = nq % n_tiles, step_dr = nq / n_tiles;
+  auto next_tile = [&](Tile& T) KVX_INLINE {
+    if (inter)
+      step_tile(step_dn, step_dr, n_tiles, row_tiles, n_ctx, ctx, T);
+    else
+      advance_tile(n_tiles, row_tiles, n_ctx, ctx, T);
+  };
   for (int i = tid; i < a.ds / 2; i += kThreads) fsl[i] = a.fs[i];
   for (int i = tid; i < a.dt / 2; i += kThreads) {
     ftl[i] = a.ft[i];
@@ -439,7 +507,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       if (++P.c == nch) {
         P.c = 0;
         ++P.ord;
-        if (P.ord < tend - tbeg) next_tile(P.T);
+        if (P.ord < ntw) next_tile(P.T);
         P.j = j0;
         P.h = h0;
         P.i0 = i00;
@@ -459,7 +527,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       return a.src[P.T.kv] + ls * a.ss.l + P.T.b * a.ss.b + P.h * a.ss.h + P.i0;
     };
     ChunkPos fpos;
-    fpos.T = decode_tile(a, tbeg);
+    fpos.T = tile_at(tfirst);
     fpos.c = 0;
     fpos.j = j0;
     fpos.h = h0;
@@ -685,7 +753,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     int sc = 0;    // s % spt
     int sord = 0;  // s / spt: tile ordinal of step s
     // tile whose rows are stored next, and the physical blocks of its rows
-    Tile stT = decode_tile(a, tbeg);
+    Tile stT = tile_at(tfirst);
     int st_ord = 0;
     int32_t blk[kRowsPerThread];
     load_blocks<PAGED>(a, stT, tid, blk);
@@ -712,7 +780,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // Rows of tile stT staged in buffer sb, then the block ids of the next.
     auto store_tile = [&](int sb) KVX_INLINE {
       store_rows<PAGED>(a, stT, lds + sb * 2 * kPlane, tid, blk);
-      if (++st_ord < tend - tbeg) next_tile(stT);
+      if (++st_ord < ntw) next_tile(stT);
       load_blocks<PAGED>(a, stT, tid, blk);
     };
     auto end_step = [&]() KVX_INLINE {
@@ -722,7 +790,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
           lds_barrier();  // staging complete
           store_tile(s & 1);
         }
-        if (bias_ord + 1 < tend - tbeg) {
+        if (bias_ord + 1 < ntw) {
           next_tile(biasT);
           ++bias_ord;
         }
@@ -882,7 +950,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     }
   };
 
-  Tile T = decode_tile(a, tbeg);
+  Tile T = tile_at(tfirst);
   Blocks B = blocks(T, cw);
   Tile Tn = T;      // next tile (decoded in the step that loads its weights)
   Blocks Bn = B;

@@ -520,8 +520,12 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       const int64_t total = int64_t(tiles) * a.n_tiles * 2 * Lt;
       if (total > INT32_MAX) return KVX_ESHAPE;
       a.total_tiles = static_cast<int32_t>(total);
+      // interleaved tile order when one tile's weight slice (din x 256 bf16)
+      // reaches 512 KiB: contiguous ranges would then keep several layers'
+      // translators in flight per XCD, more than its 4 MiB L2 holds
+      a.interleave = p->din >= 1024 ? 1 : 0;
       // persistent: one workgroup per compute unit (the kernel's LDS use
-      // allows exactly one), each walking a contiguous range of tiles
+      // allows exactly one)
       const int grid = static_cast<int>(total < p->n_cu ? total : p->n_cu);
       launch_fused(identity, Ds == 128, p->precision, grid, st, a);
     } else {
