@@ -63,6 +63,11 @@ struct kvx_plan {
   void* trash = nullptr;
   uint8_t* split_mask = nullptr; // precision BF16X2_OUTLIER: [Lt][2][din/128]
   int64_t split_ksteps = 0, ksteps = 0;
+  // fused kernel: interleaved tile order when one tile's weight slice
+  // (din x 256 bf16) reaches 512 KiB; with contiguous ranges the workgroups
+  // of an XCD would then keep several layers' translators in flight, more
+  // than its 4 MiB L2 holds
+  int32_t tile_order = 0;
   void* block = nullptr;         // single allocation backing all of the above
 };
 
@@ -160,6 +165,7 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   p->din = static_cast<int32_t>(din64);
   p->dout = static_cast<int32_t>(dout64);
   p->kernel = fused_supported(*p) ? kFused : kTiled;
+  p->tile_order = p->kernel == kFused && p->din >= 1024 ? 1 : 0;
 
   auto fail = [&](kvx_status s) {
     kvx_plan_destroy(p);
@@ -319,6 +325,7 @@ kvx_status kvx_plan_query(const kvx_plan* p, kvx_plan_info* info) {
   info->weight_bytes = p->bytes;
   info->split_ksteps = p->split_ksteps;
   info->ksteps = p->ksteps;
+  info->tile_order = p->tile_order;
   return KVX_OK;
 }
 
@@ -520,10 +527,7 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       const int64_t total = int64_t(tiles) * a.n_tiles * 2 * Lt;
       if (total > INT32_MAX) return KVX_ESHAPE;
       a.total_tiles = static_cast<int32_t>(total);
-      // interleaved tile order when one tile's weight slice (din x 256 bf16)
-      // reaches 512 KiB: contiguous ranges would then keep several layers'
-      // translators in flight per XCD, more than its 4 MiB L2 holds
-      a.interleave = p->din >= 1024 ? 1 : 0;
+      a.interleave = p->tile_order;
       // persistent: one workgroup per compute unit (the kernel's LDS use
       // allows exactly one)
       const int grid = static_cast<int>(total < p->n_cu ? total : p->n_cu);

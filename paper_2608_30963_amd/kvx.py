@@ -94,7 +94,8 @@ class FitInfo(C.Structure):
 class PlanInfo(C.Structure):
     _fields_ = [("kernel", C.c_int32), ("tile_rows", C.c_int32), ("tile_cols", C.c_int32),
                 ("threads", C.c_int32), ("precision", C.c_int32), ("weight_bytes", C.c_int64),
-                ("split_ksteps", C.c_int64), ("ksteps", C.c_int64)]
+                ("split_ksteps", C.c_int64), ("ksteps", C.c_int64),
+                ("tile_order", C.c_int32)]
 
 
 _lib = None

@@ -195,3 +195,36 @@ def test_outlier_marks_shape_is_checked():
     keep = []
     assert kvx._marks(None, src, keep) is None
     assert kvx._marks([[[1] * 8] * 2] * 2, src, keep) is not None and len(keep) == 1
+
+
+def test_struct_layouts_match_headers(tmp_path):
+    """The ctypes mirrors of the C-ABI structs have the size and field
+    offsets a C compiler gives the declarations in include/*.h (field names
+    are the C names)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    pairs = [(kvx.Model, "kvx_model"), (kvx.PlanDesc, "kvx_plan_desc"),
+             (kvx.Factors, "kvx_factors"), (kvx.IO, "kvx_io"), (kvx.PlanInfo, "kvx_plan_info"),
+             (kvx.FitDesc, "kvx_fit_desc"), (kvx.FitIO, "kvx_fit_io"),
+             (kvx.FitInfo, "kvx_fit_info")]
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "kvx.h"', '#include "kvx_fit.h"',
+             "int main(void) {"]
+    expect = []
+    for cls, cname in pairs:
+        lines.append(f'  printf("%zu\\n", sizeof({cname}));')
+        expect.append(C.sizeof(cls))
+        for f in cls._fields_:
+            lines.append(f'  printf("%zu\\n", offsetof({cname}, {f[0]}));')
+            expect.append(getattr(cls, f[0]).offset)
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    subprocess.run([gcc, "-std=c99", "-I", inc, str(src), "-o", str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], check=True, capture_output=True,
+                                          text=True).stdout.split()]
+    assert got == expect

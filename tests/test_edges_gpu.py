@@ -26,11 +26,13 @@ def _spec(**kw):
     return S.Spec(**base)
 
 
-def _check(prob, precision=kvx.KVX_PREC_BF16X2, expect_kernel=1):
+def _check(prob, precision=kvx.KVX_PREC_BF16X2, expect_kernel=1, expect_order=None):
     print(f"[edges] {prob.spec.name} T={prob.spec.src_tokens} B={prob.spec.batch} "
           f"tt={list(prob.tgt_tokens)[:8]}", flush=True)
     dev = U.DevProblem(prob, precision, cap=max(1, int(prob.tgt_tokens.max())))
     assert dev.tr.info().kernel == expect_kernel
+    if expect_order is not None:
+        assert dev.tr.info().tile_order == expect_order
     dev.run()
     U.torch().cuda.synchronize()
     rk, rv = O.translate(prob, cap=dev.cap)
@@ -83,6 +85,29 @@ def test_two_heads_per_chunk_mix2_partial_tile():
     _check(S.make_problem(dataclasses.replace(spec, name="ds64-mix2-spans", span_lo=1,
                                               span_hi=2)))
     _check(S.make_problem(spec), precision=kvx.KVX_PREC_F16)
+
+
+def test_interleaved_tile_order():
+    """din = 1024 (two mixed source layers of 4 heads x 128) selects the
+    interleaved tile order.  More work units than compute units, so each
+    workgroup steps through several of them (carries across N tile, row
+    tile, K|V and layer); dout = 384 leaves the second N tile half used.
+    Identity alignment, span maps and the F16 operand mode."""
+    spec = _spec(name="interleaved", src=S.ModelShape(4, 4, 128, 1.0e6),
+                 tgt=S.ModelShape(4, 3, 128, 1.0e4), mix=2,
+                 layer_map=(0, 1, 1, 2, 2, 3, 3, 0), src_tokens=1100, batch=3)
+    prob = S.make_problem(spec)
+    # 3 contexts x 9 row tiles x 2 N tiles x 4 layers x K|V = 432 units
+    assert 3 * 9 * 2 * 4 * 2 > 256
+    _check(prob, expect_order=1)
+    _check(prob, precision=kvx.KVX_PREC_F16, expect_order=1)
+    spans = S.make_problem(dataclasses.replace(spec, name="interleaved-spans", batch=4,
+                                               span_lo=1, span_hi=3))
+    _check(spans, expect_order=1)
+    # a shorter contraction keeps the contiguous order
+    short = S.make_problem(dataclasses.replace(spec, name="contiguous", mix=1,
+                                               layer_map=(0, 1, 2, 3), src_tokens=300))
+    _check(short, expect_order=0)
 
 
 def test_strided_source_view():

@@ -32,7 +32,8 @@ def _block_table(tt, block_size, seed, spare=5):
     return table, num_blocks
 
 
-def _run_paged(spec, block_size, precision=kvx.KVX_PREC_BF16X2, flash=False, seed=7):
+def _run_paged(spec, block_size, precision=kvx.KVX_PREC_BF16X2, flash=False, seed=7,
+               expect_order=None):
     T = U.torch()
     prob = S.make_problem(spec)
     tt = prob.tgt_tokens
@@ -40,6 +41,8 @@ def _run_paged(spec, block_size, precision=kvx.KVX_PREC_BF16X2, flash=False, see
           f"flash={flash}", flush=True)
     table, nblk = _block_table(tt, block_size, seed)
     dev = U.DevProblem(prob, precision, cap=1)
+    if expect_order is not None:
+        assert dev.tr.info().tile_order == expect_order
     Lt, Ht, Dt = spec.tgt.n_layers, spec.tgt.n_kv_heads, spec.tgt.head_dim
     tdt = T.bfloat16 if spec.dtype == S.BF16 else T.float32
     if flash:  # [Lt][num_blocks][block_size][Ht][Dt]
@@ -87,6 +90,12 @@ def test_paged_config2_flash_layout_f16():
 
 def test_paged_config3_span_map_batch():
     _run_paged(S.config(3, src_tokens=700, batch=2), block_size=32)
+
+
+def test_paged_config5_interleaved_span_map():
+    """Long contraction (3 x 1024 features): interleaved tile order, span map,
+    paged target."""
+    _run_paged(S.config(5, src_tokens=300), block_size=16, expect_order=1)
 
 
 def test_paged_config1_fp32_tiled():
