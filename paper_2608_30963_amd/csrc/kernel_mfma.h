@@ -329,26 +329,36 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
   const int npb = a.dout / 64;
   const int per_head = a.dt / 64;
   bf16_t* dst = a.tgt[Tc.kv] + Tc.l * a.ts.l;
+  // Piece i of this thread is row r = it / 32 + 8 i of the tile, staged
+  // column group (it % 32) ^ stage_swz(r), where stage_swz(r) = 8 (i % 4):
+  // the column part of its address takes four values, formed once.  A
+  // staged column group lies within one target head (the pair block's 32
+  // features and their partners dt/2 further on).
+  int64_t coff[4];
+  bool con[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int sc8 = (it % 32) ^ (8 * q);   // staged column / 8
+    const int pbw = Tc.nt * 4 + sc8 / 8;   // pair block of the owning consumer wave
+    const int half = (sc8 / 4) % 2;
+    const int hd = pbw / per_head;         // target head
+    const int d = 32 * (pbw - hd * per_head) + half * (a.dt / 2) + (sc8 % 4) * 8;
+    coff[q] = static_cast<int64_t>(hd) * a.ts.h + d;
+    con[q] = pbw < npb;  // pair blocks past dout go to the trash area
+  }
+  const int r0 = it / 32;
+  const int64_t row0 =
+      static_cast<int64_t>(Tc.b) * a.ts.b + static_cast<int64_t>(Tc.t0 + r0) * a.ts.t;
 #pragma unroll
   for (int i = 0; i < kRowsPerThread; ++i) {
-    const int pc = it + 256 * i;
-    const int r = pc / (kNT / 8);
-    const int sc8 = (pc % (kNT / 8)) ^ stage_swz(r);  // staged column / 8
-    const int w = sc8 / 8;            // owning consumer wave (pair block)
-    const int pbw = Tc.nt * 4 + w;
-    const int t = Tc.t0 + r;
-    // rows past the context's end and pair blocks past dout go to the trash
-    // area, so the store is unconditional
-    const int half = (sc8 / 4) % 2;
-    const int hpw = pbw / per_head;
-    const int colg = hpw * a.dt + 32 * (pbw % per_head) + half * (a.dt / 2) + (sc8 % 4) * 8;
-    const int hd = colg / a.dt;
-    const int d = colg % a.dt;
+    const int t = Tc.t0 + r0 + 8 * i;
     const int64_t row = PAGED ? static_cast<int64_t>(blk[i]) * a.ts.b +
                                     static_cast<int64_t>(t % a.pg.block_size) * a.ts.t
-                              : static_cast<int64_t>(Tc.b) * a.ts.b + static_cast<int64_t>(t) * a.ts.t;
-    bf16_t* q = dst + hd * a.ts.h + row + d;
-    q = (t < Tc.tt && pbw < npb) ? q : a.trash;
+                              : row0 + static_cast<int64_t>(8 * i) * a.ts.t;
+    bf16_t* q = dst + coff[i % 4] + row;
+    // rows past the context's end go to the trash area too, so the store is
+    // unconditional
+    q = (t < Tc.tt && con[i % 4]) ? q : a.trash;
     st_stream(q, *reinterpret_cast<const uint4*>(st + stage_slot(it, i)));
   }
 }
