@@ -312,10 +312,15 @@ __device__ __forceinline__ void load_blocks(const FusedArgs& a, const Tile& Tc, 
 // its next transform overwrites them, without any other thread touching them
 // in between, and the stores can run in the step after the staging.  Staged
 // column w*64 + p*32 + e holds feature c_p + e of pair block 4*nt + w.
-// The swizzle spreads the 32 rows that one staging write of a consumer wave
-// covers over the LDS banks (four times fewer bank conflicts than the plain
-// layout); a store still covers whole rows, so its coalescing is unchanged.
-__device__ __forceinline__ int stage_swz(int row) { return row & 24; }
+// The swizzle, an XOR of the column group by row bits 1-2 (placed at column
+// bits 3-4), spreads the 32 rows that one staging write of a consumer wave
+// covers over the LDS banks: a half-wave of 8-byte writes then touches each
+// bank it can reach at most twice, the least for writes that fill half of
+// each 16-byte piece.  It leaves column bit 2 alone (the consumers' second
+// 8-byte write goes to the piece owned by thread it + 4) and uses row bits
+// 0-4 only (so the stores can form a thread's column groups once).  A store
+// still covers whole rows, so its coalescing is unchanged.
+__device__ __forceinline__ int stage_swz(int row) { return (row & 6) << 2; }
 
 __device__ __forceinline__ int stage_slot(int it, int j) {
   return (j / 8) * kPlane + (it / 8 + 32 * ((j % 8) / 2)) * kLDA + 64 * (j % 2) + 8 * (it % 8);
@@ -330,15 +335,16 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
   const int per_head = a.dt / 64;
   bf16_t* dst = a.tgt[Tc.kv] + Tc.l * a.ts.l;
   // Piece i of this thread is row r = it / 32 + 8 i of the tile, staged
-  // column group (it % 32) ^ stage_swz(r), where stage_swz(r) = 8 (i % 4):
-  // the column part of its address takes four values, formed once.  A
-  // staged column group lies within one target head (the pair block's 32
-  // features and their partners dt/2 further on).
+  // column group (it % 32) ^ stage_swz(r).  stage_swz reads row bits 0-4
+  // only, and r agrees with it / 32 + 8 (i % 4) there, so the column part of
+  // the address takes at most four values, formed once.  A staged column
+  // group lies within one target head (the pair block's 32 features and
+  // their partners dt/2 further on).
   int64_t coff[4];
   bool con[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int sc8 = (it % 32) ^ (8 * q);   // staged column / 8
+    const int sc8 = (it % 32) ^ stage_swz(it / 32 + 8 * q);  // staged column / 8
     const int pbw = Tc.nt * 4 + sc8 / 8;   // pair block of the owning consumer wave
     const int half = (sc8 / 4) % 2;
     const int hd = pbw / per_head;         // target head
