@@ -1,0 +1,43 @@
+"""Host logic of bench.py (CPU only): the one-GPU contract, and the lookup
+of the committed counter summaries that roofline.traffic comes from."""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr
+    assert r.stdout == ""
+
+
+def test_recorded_traffic_follows_the_kernel_sources(tmp_path, monkeypatch):
+    # the committed headline summary matches the current sources
+    t = bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1, "contiguous")
+    assert t is not None and 3.0e8 < t < 5.0e8
+    # another precision, size or layout has no summary
+    assert bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "f16", 4096, 1, "contiguous") is None
+    assert bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 2048, 1, "contiguous") is None
+    assert bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1, "paged16") is None
+    # a changed translation source invalidates it; the fit's source does not
+    src = tmp_path / "csrc"
+    shutil.copytree(bench.KERNEL_SOURCES, src)
+    monkeypatch.setattr(bench, "KERNEL_SOURCES", str(src))
+    h0 = bench.kernel_source_hash()
+    with open(src / "fit.hip", "a") as fh:
+        fh.write("\n// edit\n")
+    assert bench.kernel_source_hash() == h0
+    with open(src / "kernel_mfma.h", "a") as fh:
+        fh.write("\n// edit\n")
+    assert bench.kernel_source_hash() != h0
+    assert bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1,
+                                  "contiguous") is None
