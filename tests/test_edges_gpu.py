@@ -97,8 +97,10 @@ def test_interleaved_tile_order():
                  tgt=S.ModelShape(4, 3, 128, 1.0e4), mix=2,
                  layer_map=(0, 1, 1, 2, 2, 3, 3, 0), src_tokens=1100, batch=3)
     prob = S.make_problem(spec)
-    # 3 contexts x 9 row tiles x 2 N tiles x 4 layers x K|V = 432 units
-    assert 3 * 9 * 2 * 4 * 2 > 256
+    # more work units (row tiles x N tiles x layers x K|V) than compute units
+    n_cu = U.torch().cuda.get_device_properties(0).multi_processor_count
+    units = sum(-(-int(t) // 128) for t in prob.tgt_tokens) * 2 * 4 * 2
+    assert units > n_cu, (units, n_cu)
     _check(prob, expect_order=1)
     _check(prob, precision=kvx.KVX_PREC_F16, expect_order=1)
     spans = S.make_problem(dataclasses.replace(spec, name="interleaved-spans", batch=4,
