@@ -658,6 +658,22 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
           for (int i = 0; i < 8; ++i)
             rope_cs(f[i], T.t0 + tid / 8 + 32 * u, csc[u][i], css[u][i]);
       }
+      // span maps: the token and weight of each row's third entry, when it
+      // has one, requested before any row's arithmetic (the entry's data is
+      // then requested in the row's turn without a dependent index load)
+      int k3[kPrefetch2 ? kUnits : 1];
+      float w3[kPrefetch2 ? kUnits : 1];
+      if constexpr (kPrefetch2) {
+#pragma unroll
+        for (int u = 0; u < kUnits; ++u) {
+          k3[u] = 0;
+          w3[u] = 0.f;
+          if (R.ri.e1[u] - R.ri.e0[u] >= 3) {
+            k3[u] = a.col_idx[R.ri.e0[u] + 2];
+            w3[u] = a.weight[R.ri.e0[u] + 2];
+          }
+        }
+      }
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
         const int r = tid / 8 + 32 * u;
@@ -709,8 +725,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         }
         if constexpr (!IDENT) {
           for (int e = R.ri.e0[u] + (kPrefetch2 ? 2 : 1); e < R.ri.e1[u]; ++e) {
-            const int k = a.col_idx[e];
-            const float w = a.weight[e];
+            const bool third = kPrefetch2 && e == R.ri.e0[u] + 2;
+            const int k = third ? k3[kPrefetch2 ? u : 0] : a.col_idx[e];
+            const float w = third ? w3[kPrefetch2 ? u : 0] : a.weight[e];
             const bf16_t* p = pg.p + k * a.ss.t;
             float x0[8], x1[8];
             unpack8(ld_src<STREAM>(p), x0);
