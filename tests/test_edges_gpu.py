@@ -75,6 +75,30 @@ def test_empty_contexts_and_rows():
     _check(prob)
 
 
+def test_long_spans():
+    """Rows pooling 3 to 7 source tokens (the fused kernel prefetches the
+    second entry, requests the third entry's index early and reads the rest
+    in its pooling loop), drawn spans and a hand-made map with entries out
+    of order, repeated, and weights of both signs; split and fp16 operand
+    precisions."""
+    spec = _spec(name="long-spans", src_tokens=700, batch=2, span_lo=3, span_hi=7)
+    prob = S.make_problem(spec)
+    _check(prob)
+    _check(prob, precision=kvx.KVX_PREC_F16)
+    rng = np.random.default_rng(11)
+    tt = np.array([90, 161], dtype=np.int32)
+    counts, cols = [], []
+    for t in tt:
+        for r in range(int(t)):
+            n = int(rng.integers(3, 8))
+            counts.append(n)
+            cols.extend(int(x) for x in rng.integers(0, spec.src_tokens, size=n))
+    row_ptr = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    weight = rng.uniform(-1.0, 1.0, size=len(cols)).astype(np.float32)
+    _check(dataclasses.replace(prob, tgt_tokens=tt, row_ptr=row_ptr,
+                               col_idx=np.array(cols, dtype=np.int32), weight=weight))
+
+
 def test_two_heads_per_chunk_mix2_partial_tile():
     """Ds = 64 (a K-chunk spans two source heads), two mixed source layers,
     and dout = 384 (the second output tile is half used)."""
