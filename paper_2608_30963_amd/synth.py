@@ -411,6 +411,27 @@ def draw_mixture(spec: Spec, n_mix: int, with_bias: bool = True):
     return alpha, ws[0], ws[1], bs[0], bs[1]
 
 
+def llama31_inv_freq(base: float, head_dim: int, factor: float = 8.0, low: float = 1.0,
+                     high: float = 4.0, original_context: int = 8192) -> np.ndarray:
+    """RoPE frequencies with the long-context rescaling published with
+    Llama 3.1 (an input table for the ``inv_freq`` override): components
+    whose wavelength 2 pi / theta is below original_context / high keep their
+    frequency, those above original_context / low are slowed by ``factor``,
+    and the band in between blends the two linearly in
+    original_context / wavelength."""
+    out = np.array([base ** (-2.0 * i / head_dim) for i in range(head_dim // 2)])
+    for i, th in enumerate(out):
+        wavelen = 2.0 * np.pi / th
+        if wavelen < original_context / high:
+            continue
+        if wavelen > original_context / low:
+            out[i] = th / factor
+            continue
+        s = (original_context / wavelen - low) / (high - low)
+        out[i] = (1.0 - s) * th / factor + s * th
+    return out
+
+
 def tiny_spec(**kw) -> Spec:
     """A small custom problem for property tests; every field overridable."""
     base = dict(cfg_id=100, name="tiny", src=ModelShape(3, 2, 8, 1.0e4),

@@ -26,6 +26,11 @@ What pins what:
   dense pooling matrix, numpy matmul) assembled independently here.
 * Input-feature order of a mixed target layer: W selecting feature
   (j*Hs + h)*Ds + d returns source layer layer_map[l*mix+j], head h, dim d.
+* Frequency override tables: a table holding base^(-2i/D) reproduces the
+  base path bit for bit; any table (the Llama 3.1 rescaled frequencies, or
+  arbitrary values) turns pair i by p * table[i], against numpy complex
+  arithmetic and against the dense expm construction of the whole operator
+  -- also on a side whose base is 0, where the table alone switches RoPE on.
 """
 from __future__ import annotations
 
@@ -57,10 +62,11 @@ def _theta(D, base):
     return np.array([base ** (-2.0 * i / D) for i in range(D // 2)])
 
 
-def _generator(D, base):
-    """Skew-symmetric generator G with exp(pG) = rotate-half RoPE at p."""
+def _generator(D, base, theta=None):
+    """Skew-symmetric generator G with exp(pG) = rotate-half RoPE at p
+    (frequencies ``theta`` if given, else base^(-2i/D))."""
     h = D // 2
-    th = _theta(D, base)
+    th = _theta(D, base) if theta is None else np.asarray(theta, dtype=np.float64)
     G = np.zeros((D, D))
     for i in range(h):
         G[i + h, i] = th[i]
@@ -68,10 +74,10 @@ def _generator(D, base):
     return G
 
 
-def _rot_expm(D, base, p):
-    if base <= 0:
+def _rot_expm(D, base, p, theta=None):
+    if base <= 0 and theta is None:
         return np.eye(D)
-    return scipy.linalg.expm(p * _generator(D, base))
+    return scipy.linalg.expm(p * _generator(D, base, theta))
 
 
 # ---------------------------------------------------------------------------
@@ -237,9 +243,9 @@ def pin_partition_of_unity(lib):
         _close(tv[0, b, 0, :T], np.broadcast_to(-c, (T, 6)), 1e-7, "const V")
 
 
-def _dense_expect(p):
+def _dense_expect(p, src_theta=None, tgt_theta=None):
     """Independent construction: expm rotations, dense pooling matrix,
-    matmul projection, expm target rotation."""
+    matmul projection, expm target rotation (frequency tables if given)."""
     spec = p.spec
     Hs, Ds = spec.src.n_kv_heads, spec.src.head_dim
     Lt, Ht, Dt = spec.tgt.n_layers, spec.tgt.n_kv_heads, spec.tgt.head_dim
@@ -251,8 +257,8 @@ def _dense_expect(p):
     xv = _f64(p.src_v, spec.dtype)
     Wk = _f64(p.w_k, spec.dtype)
     Wv = _f64(p.w_v, spec.dtype)
-    Rs = [_rot_expm(Ds, spec.src.rope_base, -k) for k in range(T)]
-    Rt = [_rot_expm(Dt, spec.tgt.rope_base, t) for t in range(cap)]
+    Rs = [_rot_expm(Ds, spec.src.rope_base, -k, src_theta) for k in range(T)]
+    Rt = [_rot_expm(Dt, spec.tgt.rope_base, t, tgt_theta) for t in range(cap)]
     row0 = 0
     for b in range(B):
         Tt = int(p.tgt_tokens[b])
@@ -340,9 +346,51 @@ def pin_rows_match_translate(lib):
         _close(rv[i], tv[l, b, :, t, :].reshape(-1), 0.0, "rows V")
 
 
+def pin_inv_freq_table(lib):
+    rng = np.random.default_rng(9)
+    # (a) a table equal to the base frequencies: the same bits as the base path
+    for D, base in [(8, 1.0e4), (128, 1.0e6), (256, 1.0e4)]:
+        x = rng.standard_normal(D)
+        for p in [3.0, 4095.0, -77.0]:
+            a = O.rope(x, p, base, inv_freq=_theta(D, base), lib_path=lib)
+            assert np.array_equal(a, O.rope(x, p, base, lib_path=lib)), "table == base^(-2i/D)"
+    spec = S.tiny_spec(src=S.ModelShape(3, 2, 8, 1.0e4), tgt=S.ModelShape(2, 2, 6, 500.0),
+                       span_lo=1, span_hi=3, src_tokens=11, bias_std=0.2)
+    p = S.make_problem(spec)
+    k0, v0 = O.translate(p, lib_path=lib)
+    k1, v1 = O.translate(p, src_inv_freq=_theta(8, 1.0e4), tgt_inv_freq=_theta(6, 500.0),
+                         lib_path=lib)
+    assert np.array_equal(k0, k1, equal_nan=True) and np.array_equal(v0, v1, equal_nan=True)
+    # (b) a rescaled table (Llama 3.1) and an arbitrary one against numpy
+    # complex rotation; the base argument differs from the table, and a base
+    # of 0 must not matter once a table is given
+    tables = [(128, S.llama31_inv_freq(5.0e5, 128)), (8, np.array([1.0, 0.3, 0.05, 0.01]))]
+    for D, th in tables:
+        x = rng.standard_normal(D)
+        h = D // 2
+        for base in (1.0e4, 0.0):
+            for p_ in [1.0, 100.0, 8191.0, -5.0]:
+                z = (x[:h] + 1j * x[h:]) * np.exp(1j * p_ * th)
+                _close(O.rope(x, p_, base, inv_freq=th, lib_path=lib),
+                       np.concatenate([z.real, z.imag]), 1e-12, f"table D={D} base={base}")
+    # (c)-(d) the whole operator with tables on both sides, one of them on a
+    # side whose base is 0, against the dense expm construction
+    ths = np.array([0.9, 0.2, 0.04, 0.001])
+    tht = np.array([1.3, 0.5, 0.07])
+    for src_base, tgt_base in [(0.0, 300.0), (100.0, 0.0)]:
+        spec = S.tiny_spec(src=S.ModelShape(3, 1, 8, src_base), tgt=S.ModelShape(2, 2, 6, tgt_base),
+                           mix=2, layer_map=(0, 2, 1, 1), span_lo=1, span_hi=3, src_tokens=6,
+                           batch=2, bias_std=0.3)
+        p = S.make_problem(spec)
+        tk, tv = O.translate(p, src_inv_freq=ths, tgt_inv_freq=tht, lib_path=lib)
+        ek, ev = _dense_expect(p, ths, tht)
+        _close(tk, ek, 1e-9, f"tables K base {src_base}/{tgt_base}")
+        _close(tv, ev, 1e-9, f"tables V base {src_base}/{tgt_base}")
+
+
 ALL_PINS = [
     pin_rope_complex, pin_rope_d2_closed_form, pin_rope_expm, pin_rope_group,
     pin_identity_translator, pin_no_rope_is_matmul, pin_linearity, pin_span_mean,
     pin_partition_of_unity, pin_dense_bruteforce, pin_mixed_feature_order,
-    pin_rows_match_translate,
+    pin_rows_match_translate, pin_inv_freq_table,
 ]

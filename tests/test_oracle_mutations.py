@@ -36,6 +36,13 @@ MUTANTS = {
                                  "int64_t col = ((int64_t)h * p->mix + j) * Ds;"),
     "v_rotated": ("s->zv[col + d] += w * s->xv[d];", "s->zv[col + d] += w * s->xr[d];"),
     "context_ignored": ("(((ls * B + b) * Hs + h)", "(((ls * B + 0) * Hs + h)"),
+    "inv_freq_index_2i": ("if (m->inv_freq) return m->inv_freq[i];",
+                          "if (m->inv_freq) return m->inv_freq[(2 * i) % (m->head_dim / 2)];"),
+    "inv_freq_as_revolutions": ("if (m->inv_freq) return m->inv_freq[i];",
+                                "if (m->inv_freq) return m->inv_freq[i] * 6.283185307179586;"),
+    "inv_freq_ignored": ("if (m->inv_freq) return m->inv_freq[i];", ""),
+    "inv_freq_needs_base": ("return m->inv_freq != NULL || m->rope_base > 0.0;",
+                            "return m->rope_base > 0.0;"),
     "span_last_dropped": ("e1 = p->row_ptr[row0 + t + 1];",
                           "e1 = p->row_ptr[row0 + t + 1] - (p->row_ptr[row0 + t + 1] > e0 + 1);"),
 }
