@@ -75,7 +75,11 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def recorded_traffic(workload: str, precision: str, src_tokens: int, batch: int, layout: str):
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def recorded_traffic(workload: str, precision: str, src_tokens: int, batch: int, layout: str,
+                     profiles: str = None):
     """HBM bytes per launch from the committed rocprofv3 counter summary of
     this workload (FETCH_SIZE and WRITE_SIZE, scaled by a copy kernel's
     reading), or None when no summary matches or the kernel sources have
@@ -83,7 +87,7 @@ def recorded_traffic(workload: str, precision: str, src_tokens: int, batch: int,
     want = {"workload": workload, "precision": precision, "src_tokens": str(src_tokens),
             "batch": str(batch), "target_layout": layout,
             "kernel_source_sha256": kernel_source_hash()}
-    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+    for path in sorted(glob.glob(os.path.join(profiles or PROFILES, "*.md"))):
         rec = {}
         with open(path) as fh:
             for line in fh:

@@ -152,15 +152,21 @@ typedef struct kvx_plan kvx_plan;
  * weights into plan-owned device memory (synchronous; uses the current HIP
  * device).  The caller's weight and bias buffers may be freed on return.
  * Errors: KVX_EINVAL (NULL/out of range), KVX_ESHAPE, KVX_EUNSUPPORTED
- * (head_dim odd), KVX_ENOMEM, KVX_EHIP.  On error *out is set to NULL. */
+ * (head_dim odd; or a plan the matrix-core kernel does not tile -- fp32, or
+ * head_dim not a multiple of 16 (source) / 64 (target) or above 512 -- whose
+ * contraction length mix*Hs*Ds exceeds 16384, the pooled rows the general
+ * kernel keeps in LDS), KVX_ENOMEM, KVX_EHIP.  On error *out is set to NULL. */
 kvx_status kvx_plan_create(const kvx_plan_desc* desc, kvx_plan** out);
 
 /* Enqueue the translation on `stream` (a hipStream_t; NULL = default stream).
  * Asynchronous: KV and alignment buffers are borrowed and must stay valid
  * until the stream work completes.  Every host-visible argument is validated
  * before anything is enqueued; device-resident CSR contents are trusted unless
- * the environment sets KVX_VALIDATE=1 (then they are copied back and checked:
- * monotone row_ptr, col_idx in range; KVX_EDATA otherwise).  batch == 0 or an
+ * the environment sets KVX_VALIDATE=1 (then, after synchronising `stream`, they
+ * are copied back and checked before any launch: row_ptr[0] == 0 and
+ * monotone, col_idx in [0, src_tokens), no empty row, and each row's weights
+ * summing to 1 within n_row * 2^-23 -- pooling rows partition unity; any
+ * violation returns KVX_EDATA with nothing enqueued).  batch == 0 or an
  * empty output is a no-op returning KVX_OK.  The plan is immutable and holds no
  * per-call scratch, so concurrent calls on different streams are safe. */
 kvx_status kvx_translate(const kvx_plan* plan, const kvx_io* io, void* stream);

@@ -94,17 +94,19 @@ extern "C" kvx_status kvx_plan_create_factored(const kvx_plan_desc* d, const kvx
     return KVX_EINVAL;
   }
 
-  // composed W_k, W_v (plan dtype) and, for a mixture, b_k, b_v (fp32)
-  const bool mixb = f->kind == KVX_FACTORS_MIXTURE && f->b_k && f->b_v;
+  // composed W_k, W_v (plan dtype) and, for a mixture, b_k and b_v (fp32),
+  // each bias composed only when its member biases are given (NULL: zero)
+  const bool mix = f->kind == KVX_FACTORS_MIXTURE;
+  const bool mixb[2] = {mix && f->b_k, mix && f->b_v};
   const size_t wbytes = size_t(nw) * esz;
   const size_t bbytes = size_t(lt) * dout * sizeof(float);
   void* buf = nullptr;
-  hipError_t e = hipMalloc(&buf, 2 * wbytes + (mixb ? 2 * bbytes : 0));
+  hipError_t e = hipMalloc(&buf, 2 * wbytes + 2 * bbytes);
   if (e != hipSuccess) return hip_status(e);
   char* base = static_cast<char*>(buf);
   void* w[2] = {base, base + wbytes};
-  float* b[2] = {mixb ? reinterpret_cast<float*>(base + 2 * wbytes) : nullptr,
-                 mixb ? reinterpret_cast<float*>(base + 2 * wbytes + bbytes) : nullptr};
+  float* b[2] = {mixb[0] ? reinterpret_cast<float*>(base + 2 * wbytes) : nullptr,
+                 mixb[1] ? reinterpret_cast<float*>(base + 2 * wbytes + bbytes) : nullptr};
   if (f->kind == KVX_FACTORS_LOWRANK) {
     const void* U[2] = {f->u_k, f->u_v};
     const void* V[2] = {f->v_k, f->v_v};
@@ -138,13 +140,11 @@ extern "C" kvx_status kvx_plan_create_factored(const kvx_plan_desc* d, const kvx
         compose_mixture<bf16_t, bf16_t><<<blocks, dim3(256)>>>(
             static_cast<const bf16_t*>(W[kv]), static_cast<bf16_t*>(w[kv]), nw, m);
     }
-    if (mixb) {
-      const float* B[2] = {f->b_k, f->b_v};
-      const int64_t nb = lt * dout;
-      const unsigned bb = static_cast<unsigned>(std::min<int64_t>((nb + 255) / 256, 65536));
-      for (int kv = 0; kv < 2; ++kv)
-        compose_mixture<float, float><<<bb, dim3(256)>>>(B[kv], b[kv], nb, m);
-    }
+    const float* B[2] = {f->b_k, f->b_v};
+    const int64_t nb = lt * dout;
+    const unsigned bb = static_cast<unsigned>(std::min<int64_t>((nb + 255) / 256, 65536));
+    for (int kv = 0; kv < 2; ++kv)
+      if (mixb[kv]) compose_mixture<float, float><<<bb, dim3(256)>>>(B[kv], b[kv], nb, m);
   }
   e = hipGetLastError();
   if (e == hipSuccess) e = hipDeviceSynchronize();

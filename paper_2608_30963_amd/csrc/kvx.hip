@@ -95,9 +95,20 @@ std::vector<double> rope_table(const kvx_model& m) {
 bool fused_supported(const kvx_plan& p) {
   return p.dtype == KVX_BF16 && p.src.head_dim % 16 == 0 && p.din % 128 == 0 &&
          p.tgt.head_dim % 64 == 0 && p.dout % 64 == 0 &&
-         p.src.head_dim / 2 <= kMaxHalfDim &&
+         p.src.head_dim / 2 <= kMaxHalfDim && p.tgt.head_dim / 2 <= kMaxHalfDim &&
          int64_t(p.tgt.n_layers) * p.mix <= kMaxLayerMap;
 }
+
+// Target rows per workgroup of the tiled kernel, and the LDS its pooled rows
+// take (rows x din fp32).
+int tiled_rows(int din) {
+  int r = 16384 / (din > 0 ? din : 1);
+  return r < 1 ? 1 : (r > 16 ? 16 : r);
+}
+// dynamic LDS a launch gets without raising the kernel's limit (64 KiB):
+// din <= 16384
+constexpr size_t kMaxLdsBytes = 64 * 1024;
+size_t tiled_lds_bytes(int din) { return size_t(tiled_rows(din)) * din * sizeof(float); }
 
 // Input feature held in K-slot `k` of the fused kernel: chunk c = k / 128 holds
 // the RoPE pairs 64c .. 64c+63 of the flattened (mixed layer, head, d < Ds/2)
@@ -165,6 +176,11 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
   p->din = static_cast<int32_t>(din64);
   p->dout = static_cast<int32_t>(dout64);
   p->kernel = fused_supported(*p) ? kFused : kTiled;
+  // the tiled kernel holds one pooled row (din fp32) per target row in LDS
+  if (p->kernel == kTiled && tiled_lds_bytes(p->din) > kMaxLdsBytes) {
+    delete p;
+    return KVX_EUNSUPPORTED;
+  }
   p->tile_order = p->kernel == kFused && p->din >= 1024 ? 1 : 0;
 
   auto fail = [&](kvx_status s) {
@@ -342,11 +358,6 @@ void launch_fused(bool identity, bool ds128, int precision, int grid, hipStream_
   }
 }
 
-int tiled_rows(int din) {
-  int r = 16384 / (din > 0 ? din : 1);
-  return r < 1 ? 1 : (r > 16 ? 16 : r);
-}
-
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 // Host-side check of device CSR contents (validation mode only).
@@ -367,6 +378,21 @@ kvx_status validate_csr(const kvx_io& io, int64_t rows, hipStream_t st) {
   }
   for (int64_t i = 0; i < nnz; ++i)
     if (ci[i] < 0 || ci[i] >= io.src_tokens) return KVX_EDATA;
+  // Pooling rows are a partition of unity: no empty row, and the weights of
+  // each row sum to 1 within the rounding of its entries (each weight an fp32
+  // value, so |sum - 1| <= n_row * 2^-23 for weights that round 1/n_row).
+  std::vector<float> wv(nnz > 0 ? nnz : 1);
+  if (nnz > 0) {
+    e = hipMemcpy(wv.data(), io.weight, nnz * sizeof(float), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  for (int64_t r = 0; r < rows; ++r) {
+    const int64_t n = int64_t(rp[r + 1]) - rp[r];
+    if (n == 0) return KVX_EDATA;
+    double sum = 0.0;
+    for (int64_t i = rp[r]; i < rp[r + 1]; ++i) sum += double(wv[i]);
+    if (!(std::fabs(sum - 1.0) <= double(n) * std::ldexp(1.0, -23))) return KVX_EDATA;
+  }
   return KVX_OK;
 }
 
@@ -533,7 +559,7 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       const int grid = static_cast<int>(total < p->n_cu ? total : p->n_cu);
       launch_fused(identity, Ds == 128, p->precision, grid, st, a);
     } else {
-      const size_t lds = size_t(rows_per_tile) * p->din * sizeof(float);
+      const size_t lds = tiled_lds_bytes(p->din);
       if (p->dtype == KVX_F32) {
         TiledArgs<float> a{};
         a.src[0] = reinterpret_cast<const float*>(sk);

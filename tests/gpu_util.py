@@ -6,9 +6,12 @@ layer's K or V):
 * bf16: element-wise |g - r| <= 2e-2 * max(1, |r|) and relative Frobenius
   error <= 1e-2.  The literal max-abs bound cannot hold for bf16 outputs above
   |r| = 8 (half an ulp there is 2^-5 > 2e-2), so it scales with |r| beyond 1.
-* fp32: the same form with 1e-5.
-Integer work (layer map, alignment, head/token indexing) is checked bit-exact
-by the probe tests.
+  A tighter guard in bf16 ulps (``ulp_bound``) catches accuracy regressions
+  well inside that envelope.
+* fp32: the literal bounds, |g - r| <= 1e-5 element-wise and relative
+  Frobenius error <= 1e-5.
+Integer work (layer map, layer mixing, alignment, head/token indexing) is
+checked bit-exact by ``test_probes_gpu.py``.
 """
 from __future__ import annotations
 
@@ -44,12 +47,14 @@ class DevProblem:
     """Device copies of a problem's arrays plus a plan."""
 
     def __init__(self, prob: S.Problem, precision=kvx.KVX_PREC_BF16X2, cap=None, fill=None,
-                 lowrank=None, mixture=None, outliers=None):
+                 lowrank=None, mixture=None, outliers=None, src_inv_freq=None,
+                 tgt_inv_freq=None):
         """``lowrank=(u_k, v_k, u_v, v_v)`` or ``mixture=(alpha, w_k, w_v, b_k,
         b_v)`` (host arrays in the storage dtype, biases fp32) build the plan
         from translator factors instead of the problem's dense weights;
         ``outliers=(marks_k, marks_v)`` are the source outlier channels of
-        precision KVX_PREC_BF16X2_OUTLIER."""
+        precision KVX_PREC_BF16X2_OUTLIER; ``src_inv_freq`` / ``tgt_inv_freq``
+        override the RoPE frequencies of a side."""
         T = torch()
         spec = prob.spec
         self.prob = prob
@@ -79,7 +84,8 @@ class DevProblem:
         if outliers is not None:
             kw["outlier_k"], kw["outlier_v"] = outliers
         self.tr = kvx.Translator(spec.src, spec.tgt, spec.mix, spec.layer_map, self.kdtype,
-                                 b_k=self.b_k, b_v=self.b_v, precision=precision, **kw)
+                                 b_k=self.b_k, b_v=self.b_v, precision=precision,
+                                 src_inv_freq=src_inv_freq, tgt_inv_freq=tgt_inv_freq, **kw)
         self.cap = prob.tgt_capacity if cap is None else cap
         shape = (spec.tgt.n_layers, spec.batch, spec.tgt.n_kv_heads, self.cap,
                  spec.tgt.head_dim)
@@ -99,21 +105,56 @@ class DevProblem:
         self.tr.close()
 
 
-def check_close(got: np.ndarray, ref: np.ndarray, dtype: str, what: str):
-    """Element-wise and relative-Frobenius check; returns the metrics."""
+def bf16_ulp(x: np.ndarray) -> np.ndarray:
+    """Spacing of bfloat16 numbers at |x| (8 significant bits; subnormal
+    spacing 2^-133 below the smallest normal 2^-126)."""
+    ax = np.abs(np.asarray(x, dtype=np.float64))
+    e = np.floor(np.log2(np.maximum(ax, 2.0 ** -126)))
+    return np.exp2(e - 7)
+
+
+def ulp_metrics(got: np.ndarray, ref: np.ndarray):
+    """Worst error in bf16 ulps of the reference value (``ulp``), and the same
+    with the ulp taken at max(|r|, rms(r) / 16) (``ulp_floor``): near-zero
+    outputs of a long contraction carry an absolute error set by the size of
+    its terms, which the floored measure reads on the tensor's own scale."""
+    if got.size == 0:
+        return 0.0, 0.0
+    d = np.abs(got - ref)
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    u = float((d / bf16_ulp(ref)).max())
+    uf = float((d / bf16_ulp(np.maximum(np.abs(ref), rms / 16))).max())
+    return u, uf
+
+
+def check_close(got: np.ndarray, ref: np.ndarray, dtype: str, what: str, ulp_bound=None):
+    """Element-wise and relative-Frobenius check; returns the metrics.
+
+    bf16: ``ulp_bound`` (if given) also bounds the floored ulp error (see
+    ulp_metrics).  fp32: the element bound is the literal absolute one."""
     el, fro = TOL[dtype]
     assert got.shape == ref.shape, (what, got.shape, ref.shape)
     assert np.isfinite(got).all(), f"{what}: non-finite output"
     d = np.abs(got - ref)
-    scaled = d / np.maximum(1.0, np.abs(ref))
+    if dtype == S.F32:
+        scaled = d
+    else:
+        scaled = d / np.maximum(1.0, np.abs(ref))
     worst = float(scaled.max()) if d.size else 0.0
     rf = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300)) if d.size else 0.0
     assert worst <= el, f"{what}: element error {worst:.3e} > {el} (max abs {d.max():.3e})"
     assert rf <= fro, f"{what}: relative Frobenius {rf:.3e} > {fro}"
-    return {"max_scaled": worst, "max_abs": float(d.max()) if d.size else 0.0, "rel_fro": rf}
+    m = {"max_scaled": worst, "max_abs": float(d.max()) if d.size else 0.0, "rel_fro": rf}
+    if dtype == S.BF16:
+        m["ulp"], m["ulp_floor"] = ulp_metrics(got, ref)
+        if ulp_bound is not None:
+            assert m["ulp_floor"] <= ulp_bound, \
+                f"{what}: {m['ulp_floor']:.3f} bf16 ulps > {ulp_bound}"
+    return m
 
 
-def check_full(dev: DevProblem, ref_k: np.ndarray, ref_v: np.ndarray, what: str):
+def check_full(dev: DevProblem, ref_k: np.ndarray, ref_v: np.ndarray, what: str,
+               ulp_bound=None):
     """Compare every valid row of every target layer against the oracle."""
     spec = dev.spec
     gk = dev_to_f64(dev.tgt_k, spec.dtype)
@@ -124,5 +165,15 @@ def check_full(dev: DevProblem, ref_k: np.ndarray, ref_v: np.ndarray, what: str)
         for name, g, r in (("K", gk, ref_k), ("V", gv, ref_v)):
             gs = np.concatenate([g[l, b, :, :tt[b]].reshape(-1) for b in range(spec.batch)])
             rs = np.concatenate([r[l, b, :, :tt[b]].reshape(-1) for b in range(spec.batch)])
-            out.append(check_close(gs, rs, spec.dtype, f"{what} layer {l} {name}"))
+            out.append(check_close(gs, rs, spec.dtype, f"{what} layer {l} {name}", ulp_bound))
+    return out
+
+
+def summarize(metrics, what: str) -> dict:
+    """Worst of each metric over a list of check_close results; printed, so
+    that a test run reports the literal max-abs and ulp errors it saw."""
+    keys = ("max_abs", "max_scaled", "rel_fro", "ulp", "ulp_floor")
+    out = {k: max(m[k] for m in metrics) for k in keys if metrics and k in metrics[0]}
+    print(f"[accuracy] {what}: " + ", ".join(f"{k} {v:.3e}" for k, v in out.items()),
+          flush=True)
     return out

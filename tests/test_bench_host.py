@@ -21,13 +21,21 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_recorded_traffic_follows_the_kernel_sources(tmp_path, monkeypatch):
-    # the committed headline summary matches the current sources
-    t = bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1, "contiguous")
-    assert t is not None and 3.0e8 < t < 5.0e8
+    # a counter summary recorded for the current sources is found by its keys
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    keys = {"workload": "qwen2.5-7b->qwen2.5-1.5b", "precision": "bf16x2", "src_tokens": "4096",
+            "batch": "1", "target_layout": "contiguous",
+            "kernel_source_sha256": bench.kernel_source_hash(),
+            "traffic_bytes_per_launch": "370097794"}
+    (prof / "fused_kernel_x.md").write_text(
+        "# summary\n\n" + "".join(f"- `{k}`: `{v}`\n" for k, v in keys.items()))
+    look = lambda *a: bench.recorded_traffic(*a, profiles=str(prof))  # noqa: E731
+    assert look("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1, "contiguous") == 370097794
     # another precision, size or layout has no summary
-    assert bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "f16", 4096, 1, "contiguous") is None
-    assert bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 2048, 1, "contiguous") is None
-    assert bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1, "paged16") is None
+    assert look("qwen2.5-7b->qwen2.5-1.5b", "f16", 4096, 1, "contiguous") is None
+    assert look("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 2048, 1, "contiguous") is None
+    assert look("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1, "paged16") is None
     # a changed translation source invalidates it; the fit's source does not
     src = tmp_path / "csrc"
     shutil.copytree(bench.KERNEL_SOURCES, src)
@@ -39,5 +47,13 @@ def test_recorded_traffic_follows_the_kernel_sources(tmp_path, monkeypatch):
     with open(src / "kernel_mfma.h", "a") as fh:
         fh.write("\n// edit\n")
     assert bench.kernel_source_hash() != h0
-    assert bench.recorded_traffic("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1,
-                                  "contiguous") is None
+    assert look("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1, "contiguous") is None
+
+
+def test_committed_summaries_are_parsable():
+    """Every committed fused-kernel summary carries the keys the lookup reads."""
+    import glob
+    for path in glob.glob(os.path.join(ROOT, "profiles", "fused_kernel_*.md")):
+        text = open(path).read()
+        for k in ("workload", "precision", "src_tokens", "kernel_source_sha256"):
+            assert f"- {k}: " in text, (path, k)

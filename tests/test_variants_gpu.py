@@ -233,6 +233,17 @@ def test_mixture_bf16(precision):
         _check_variant(dev, prob, mixture=m)
 
 
+def test_mixture_bias_on_one_side_only():
+    """Member biases for one side only (the other side's pointer NULL): that
+    side gets the composed bias, the other none."""
+    spec = _spec(name="mixture-one-bias", span_lo=1, span_hi=3)
+    prob = S.make_problem(spec)
+    alpha, wk, wv, bk, bv = S.draw_mixture(spec, 3, with_bias=True)
+    for m in ((alpha, wk, wv, bk, None), (alpha, wk, wv, None, bv)):
+        dev = _run(prob, mixture=m)
+        _check_variant(dev, prob, mixture=m)
+
+
 def test_mixture_f32_and_max_members():
     spec = _f32_spec(name="mixture-f32")
     prob = S.make_problem(spec)
