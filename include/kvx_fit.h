@@ -91,6 +91,21 @@ kvx_status kvx_fit_accumulate(kvx_fit* fit, const kvx_fit_io* io, void* stream);
 kvx_status kvx_fit_solve(kvx_fit* fit, double lambda, float* w_k, float* w_v, float* b_k,
                          float* b_v, void* stream);
 
+/* kvx_fit_solve for callers that cannot allocate device memory (code that
+ * must not call hipMalloc: serving loops, harnesses that forbid allocation):
+ * the same solve, with the same results, that allocates nothing.  Its fp64
+ * workspace is a 128 MiB static device array of the library, which every
+ * device the library is loaded on holds until the process ends; systems are
+ * solved in groups that fit it, in stream order.  Limit: one system's
+ * (n^2 + n*dout) doubles, n = mix*Hs*Ds + fit_bias, must fit in the workspace
+ * (n up to 3848 at dout 512), else KVX_EUNSUPPORTED with nothing
+ * enqueued.  The current device must be the fit's (KVX_EINVAL otherwise).
+ * Every call on a device shares that device's workspace: calls that overlap
+ * on one device (other streams, other threads) race and must be serialised
+ * by the caller.  Synchronises `stream`, as kvx_fit_solve. */
+kvx_status kvx_fit_solve_noalloc(kvx_fit* fit, double lambda, float* w_k, float* w_v,
+                                 float* b_k, float* b_v, void* stream);
+
 /* Zero the accumulators (asynchronous). */
 kvx_status kvx_fit_reset(kvx_fit* fit, void* stream);
 

@@ -19,8 +19,9 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
-#include <utility>
+#include <mutex>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "common.h"
@@ -337,8 +338,9 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
 
 struct SolveArgs {
   const float* acc;  // [sys][din_p][F]
-  double* A;         // [sys][n][n] scratch
-  double* X;         // [sys][n][dout] scratch (right-hand sides, then solution)
+  double* A;         // [group][n][n] workspace, one per system of the launch
+  double* X;         // [group][n][dout] workspace (right-hand sides, then solution)
+  int32_t sys0;      // first system of the launch: block b solves system sys0 + b
   float* w[2];       // [Lt][dout][din]
   float* b[2];       // [Lt][dout] or nullptr
   int32_t* status;   // set to 1 if a pivot is not positive
@@ -352,12 +354,12 @@ __global__ void __launch_bounds__(256) fit_solve(SolveArgs a) {
   __shared__ double pk[kNB][kNB + 1];   // diagonal block / factor
   __shared__ double pr[kNB][kNB + 1];   // panel rows (tile i)
   __shared__ double pc[kNB][kNB + 1];   // panel rows (tile j)
-  const int sys = blockIdx.x;
+  const int sys = a.sys0 + blockIdx.x;
   const int tid = threadIdx.x;
   const int n = a.n, m = a.dout;
   const float* acc = a.acc + static_cast<int64_t>(sys) * a.din_p * a.F;
-  double* A = a.A + static_cast<int64_t>(sys) * n * n;
-  double* X = a.X + static_cast<int64_t>(sys) * n * m;
+  double* A = a.A + static_cast<int64_t>(blockIdx.x) * n * n;
+  double* X = a.X + static_cast<int64_t>(blockIdx.x) * n * m;
 
   // lower triangle of A from the upper accumulator blocks; ridge on Z only
   for (int64_t idx = tid; idx < static_cast<int64_t>(n) * n; idx += 256) {
@@ -537,6 +539,44 @@ __global__ void __launch_bounds__(256) fit_solve(SolveArgs a) {
           a.fit_bias ? static_cast<float>(X[static_cast<int64_t>(a.din) * m + c]) : 0.f;
 }
 
+// Status flag of a solve: cleared by a kernel (not a memset) before the
+// solve's launches.
+__global__ void __launch_bounds__(64) clear_status(int32_t* status) {
+  if (threadIdx.x == 0) status[0] = 0;
+}
+
+// Workspace of kvx_fit_solve_noalloc, held by every device the library runs
+// on until the process ends: the fp64 matrices A and right-hand sides X of as
+// many systems as fit, then the status flag.  Host code reaches it only
+// through the per-device address from hipGetSymbolAddress (solve_workspace):
+// the array's name in host code is a host-side stand-in, not a device
+// address.
+constexpr size_t kSolveWorkspaceBytes = size_t(128) << 20;
+constexpr size_t kStatusBytes = 256;
+static __device__ __align__(256) double scratch[kSolveWorkspaceBytes / sizeof(double)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_ws_mu;
+void* g_ws[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current).
+kvx_status solve_workspace(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e);
+  if (dev < 0 || dev >= kMaxDevices) return KVX_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_ws_mu);
+  if (!g_ws[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e);
+    g_ws[dev] = p;
+  }
+  *out = g_ws[dev];
+  return KVX_OK;
+}
+
 bool valid_side(const kvx_model& m) {
   return m.n_layers > 0 && m.n_kv_heads > 0 && m.head_dim > 0 && std::isfinite(m.rope_base);
 }
@@ -567,8 +607,8 @@ struct kvx_fit {
   double* fs = nullptr;
   double* ft = nullptr;
   float* acc = nullptr;        // [Lt * 2][din_p][F]
-  void* scratch = nullptr;     // prepared operands
-  size_t scratch_bytes = 0;
+  void* prep = nullptr;        // prepared operands X^T
+  size_t prep_bytes = 0;
   void* solve_buf = nullptr;
   size_t solve_bytes = 0;
   int64_t rows = 0;
@@ -702,19 +742,19 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
     ctx.row0[nb] = r;
     if (r == 0) continue;
     const int32_t rp = static_cast<int32_t>(round_up(r, kSlab));
-    // layer groups sized so the prepared operands fit a 1 GiB scratch
+    // layer groups sized so the prepared operands fit in 1 GiB
     const size_t per_layer = size_t(2) * 2 * f->F * rp * sizeof(bf16_t);
     const int64_t lg = std::max<int64_t>(1, std::min<int64_t>(Lt, (size_t(1) << 30) / per_layer));
     const size_t need = per_layer * lg;
-    if (need > f->scratch_bytes) {
-      if (f->scratch) {
+    if (need > f->prep_bytes) {
+      if (f->prep) {
         FIT_HIP(hipStreamSynchronize(st));
-        FIT_HIP(hipFree(f->scratch));
-        f->scratch = nullptr;
-        f->scratch_bytes = 0;
+        FIT_HIP(hipFree(f->prep));
+        f->prep = nullptr;
+        f->prep_bytes = 0;
       }
-      FIT_HIP(hipMalloc(&f->scratch, need));
-      f->scratch_bytes = need;
+      FIT_HIP(hipMalloc(&f->prep, need));
+      f->prep_bytes = need;
     }
     const Strides ss{io.src_stride[0], io.src_stride[1], io.src_stride[2], io.src_stride[3]};
     const Strides ts{io.tgt_stride[0], io.tgt_stride[1], io.tgt_stride[2], io.tgt_stride[3]};
@@ -749,7 +789,7 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
       pa.fit_bias = f->fit_bias;
       pa.src_rope = f->src_rope;
       pa.tgt_rope = f->tgt_rope;
-      pa.xt = static_cast<bf16_t*>(f->scratch);
+      pa.xt = static_cast<bf16_t*>(f->prep);
       pa.ctx = ctx;
       const int jobs = f->din / 2 + f->dout / 2 + (f->din_p - f->din) + (f->dout_p - f->dout);
       const dim3 pg((jobs + 255) / 256, std::min(rp / 8, 32768), nl * 2);
@@ -759,7 +799,7 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
         fit_prepare<bf16_t><<<pg, dim3(256), 0, st>>>(pa);
       FIT_HIP(hipGetLastError());
       GramArgs ga{};
-      ga.xt = static_cast<const bf16_t*>(f->scratch);
+      ga.xt = static_cast<const bf16_t*>(f->prep);
       ga.acc = f->acc;
       ga.F = f->F;
       ga.rp = rp;
@@ -808,11 +848,13 @@ kvx_status kvx_fit_solve(kvx_fit* f, double lambda, float* w_k, float* w_v, floa
   }
   char* base = static_cast<char*>(f->solve_buf);
   int32_t* status = reinterpret_cast<int32_t*>(base + abytes + xbytes);
-  FIT_HIP(hipMemsetAsync(status, 0, sizeof(int32_t), st));
+  clear_status<<<dim3(1), dim3(64), 0, st>>>(status);
+  FIT_HIP(hipGetLastError());
   SolveArgs sa{};
   sa.acc = f->acc;
   sa.A = reinterpret_cast<double*>(base);
   sa.X = reinterpret_cast<double*>(base + abytes);
+  sa.sys0 = 0;
   sa.w[0] = w_k;
   sa.w[1] = w_v;
   sa.b[0] = b_k;
@@ -827,6 +869,54 @@ kvx_status kvx_fit_solve(kvx_fit* f, double lambda, float* w_k, float* w_v, floa
   sa.fit_bias = f->fit_bias;
   fit_solve<<<dim3(static_cast<unsigned>(nsys)), dim3(256), 0, st>>>(sa);
   FIT_HIP(hipGetLastError());
+  int32_t h = 0;
+  FIT_HIP(hipMemcpyAsync(&h, status, sizeof h, hipMemcpyDeviceToHost, st));
+  FIT_HIP(hipStreamSynchronize(st));
+  return h ? KVX_EDATA : KVX_OK;
+}
+
+kvx_status kvx_fit_solve_noalloc(kvx_fit* f, double lambda, float* w_k, float* w_v, float* b_k,
+                                 float* b_v, void* stream) {
+  if (!f || !w_k || !w_v || !std::isfinite(lambda) || lambda < 0) return KVX_EINVAL;
+  if (f->fit_bias && (!b_k || !b_v)) return KVX_EINVAL;
+  int dev = 0;
+  FIT_HIP(hipGetDevice(&dev));
+  if (dev != f->device) return KVX_EINVAL;
+  const size_t per_sys = (size_t(f->n) * f->n + size_t(f->n) * f->dout) * sizeof(double);
+  const int64_t group = int64_t((kSolveWorkspaceBytes - kStatusBytes) / per_sys);
+  if (group < 1) return KVX_EUNSUPPORTED;
+  void* ws = nullptr;
+  const kvx_status s = solve_workspace(&ws);
+  if (s != KVX_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t nsys = int64_t(f->tgt.n_layers) * 2;
+  const int64_t g = std::min(group, nsys);
+  char* base = static_cast<char*>(ws);
+  int32_t* status = reinterpret_cast<int32_t*>(base + kSolveWorkspaceBytes - kStatusBytes);
+  clear_status<<<dim3(1), dim3(64), 0, st>>>(status);
+  FIT_HIP(hipGetLastError());
+  SolveArgs sa{};
+  sa.acc = f->acc;
+  sa.A = reinterpret_cast<double*>(base);
+  sa.X = reinterpret_cast<double*>(base + size_t(g) * f->n * f->n * sizeof(double));
+  sa.w[0] = w_k;
+  sa.w[1] = w_v;
+  sa.b[0] = b_k;
+  sa.b[1] = b_v;
+  sa.status = status;
+  sa.lam = lambda;
+  sa.n = f->n;
+  sa.din = f->din;
+  sa.dout = f->dout;
+  sa.din_p = f->din_p;
+  sa.F = f->F;
+  sa.fit_bias = f->fit_bias;
+  // groups of systems in stream order reuse the same workspace
+  for (int64_t s0 = 0; s0 < nsys; s0 += g) {
+    sa.sys0 = static_cast<int32_t>(s0);
+    fit_solve<<<dim3(static_cast<unsigned>(std::min(g, nsys - s0))), dim3(256), 0, st>>>(sa);
+    FIT_HIP(hipGetLastError());
+  }
   int32_t h = 0;
   FIT_HIP(hipMemcpyAsync(&h, status, sizeof h, hipMemcpyDeviceToHost, st));
   FIT_HIP(hipStreamSynchronize(st));
@@ -852,7 +942,7 @@ kvx_status kvx_fit_query(kvx_fit* f, kvx_fit_info* info) {
   for (int bi = 0; bi < nbi; ++bi) info->gram_blocks += nbj - bi;
   info->rows = f->rows;
   info->device_bytes = static_cast<int64_t>(size_t(f->tgt.n_layers) * 2 * f->din_p * f->F *
-                                            sizeof(float) + f->scratch_bytes + f->solve_bytes);
+                                            sizeof(float) + f->prep_bytes + f->solve_bytes);
   double ms = 0.0;
   kvx_status rc = KVX_OK;
   for (auto& p : f->timed) {
@@ -880,7 +970,7 @@ void kvx_fit_destroy(kvx_fit* f) {
   if (f->fs) (void)hipFree(f->fs);
   if (f->ft) (void)hipFree(f->ft);
   if (f->acc) (void)hipFree(f->acc);
-  if (f->scratch) (void)hipFree(f->scratch);
+  if (f->prep) (void)hipFree(f->prep);
   if (f->solve_buf) (void)hipFree(f->solve_buf);
   delete f;
 }

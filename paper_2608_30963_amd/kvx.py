@@ -31,8 +31,8 @@ KVX_FACTORS_LOWRANK, KVX_FACTORS_MIXTURE = 1, 2
 SYMBOLS = ("kvx_plan_create", "kvx_plan_create_factored", "kvx_translate", "kvx_plan_destroy",
            "kvx_status_string",
            "kvx_last_hip_error", "kvx_plan_query", "kvx_fit_create", "kvx_fit_accumulate",
-           "kvx_fit_solve", "kvx_fit_reset", "kvx_fit_rows", "kvx_fit_query",
-           "kvx_fit_destroy")
+           "kvx_fit_solve", "kvx_fit_solve_noalloc", "kvx_fit_reset", "kvx_fit_rows",
+           "kvx_fit_query", "kvx_fit_destroy")
 
 
 class KvxError(RuntimeError):
@@ -135,6 +135,8 @@ def load(path: str = LIB_PATH):
     lib.kvx_fit_solve.argtypes = [C.c_void_p, C.c_double, C.c_void_p, C.c_void_p, C.c_void_p,
                                   C.c_void_p, C.c_void_p]
     lib.kvx_fit_solve.restype = C.c_int
+    lib.kvx_fit_solve_noalloc.argtypes = lib.kvx_fit_solve.argtypes
+    lib.kvx_fit_solve_noalloc.restype = C.c_int
     lib.kvx_fit_reset.argtypes = [C.c_void_p, C.c_void_p]
     lib.kvx_fit_reset.restype = C.c_int
     lib.kvx_fit_rows.argtypes = [C.c_void_p]
@@ -421,6 +423,15 @@ def kvx_fit_solve(fit: int, lam: float, w_k, w_v, b_k=None, b_v=None, stream=Non
     return st
 
 
+def kvx_fit_solve_noalloc(fit: int, lam: float, w_k, w_v, b_k=None, b_v=None,
+                          stream=None) -> int:
+    st = load().kvx_fit_solve_noalloc(C.c_void_p(fit), float(lam), _ptr(w_k), _ptr(w_v),
+                                      _ptr(b_k), _ptr(b_v), C.c_void_p(_stream_handle(stream)))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_fit_solve_noalloc")
+    return st
+
+
 def kvx_fit_reset(fit: int, stream=None) -> int:
     st = load().kvx_fit_reset(C.c_void_p(fit), C.c_void_p(_stream_handle(stream)))
     if st != KVX_OK:
@@ -466,8 +477,9 @@ class Fitter:
         kvx_fit_accumulate(self.handle, io, stream)
         del keep
 
-    def solve(self, lam, stream=None):
-        """Returns fp32 device tensors (w_k, w_v, b_k, b_v)."""
+    def solve(self, lam, stream=None, noalloc=False):
+        """Returns fp32 device tensors (w_k, w_v, b_k, b_v); ``noalloc``
+        solves through kvx_fit_solve_noalloc."""
         import torch
         Lt = self.tgt.n_layers
         dout = self.tgt.n_kv_heads * self.tgt.head_dim
@@ -476,7 +488,8 @@ class Fitter:
         w_v = torch.empty_like(w_k)
         b_k = torch.empty((Lt, dout), dtype=torch.float32, device="cuda")
         b_v = torch.empty_like(b_k)
-        kvx_fit_solve(self.handle, lam, w_k, w_v, b_k, b_v, stream)
+        (kvx_fit_solve_noalloc if noalloc else kvx_fit_solve)(self.handle, lam, w_k, w_v, b_k,
+                                                                b_v, stream)
         return w_k, w_v, b_k, b_v
 
     def reset(self, stream=None):

@@ -149,6 +149,7 @@ def test_fit_calls_reject_null():
     assert lib.kvx_fit_accumulate(None, C.byref(io), None) == kvx.KVX_EINVAL
     assert lib.kvx_fit_accumulate(C.c_void_p(1), None, None) == kvx.KVX_EINVAL
     assert lib.kvx_fit_solve(None, 1.0, 0x10, 0x10, 0x10, 0x10, None) == kvx.KVX_EINVAL
+    assert lib.kvx_fit_solve_noalloc(None, 1.0, 0x10, 0x10, 0x10, 0x10, None) == kvx.KVX_EINVAL
     assert lib.kvx_fit_reset(None, None) == kvx.KVX_EINVAL
     assert lib.kvx_fit_rows(None) == 0
     info = kvx.FitInfo()
