@@ -234,7 +234,10 @@ typedef struct {
    * tile, N tile) work units.  0 = contiguous ranges (K and V alternate
    * within a workgroup); 1 = interleaved (each XCD's range dealt
    * round-robin, so the XCD's workgroups share one translator slice in its
-   * L2), chosen when din >= 1024.  0 for the tiled kernel. */
+   * L2), chosen when din >= 1024; 2 = resident (for span maps: a row tile's
+   * pooled, de-rotated rows are formed once and kept in LDS for all of its
+   * N tiles), chosen when din <= 256 and dout > 256 -- identity-aligned
+   * calls of such a plan use 0.  0 for the tiled kernel. */
   int32_t tile_order;
 } kvx_plan_info;
 

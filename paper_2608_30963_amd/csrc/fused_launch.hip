@@ -9,23 +9,37 @@
 namespace kvx {
 namespace {
 
-template <int PREC, bool STREAM, bool PAGED, bool INTER>
+template <int PREC, bool STREAM, bool PAGED, int ORDER>
 void launch_pspi(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
-  if (identity && ds128)
-    fused_kernel<true, true, PREC, STREAM, PAGED, INTER><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
-  else if (identity)
-    fused_kernel<true, false, PREC, STREAM, PAGED, INTER><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
-  else
-    fused_kernel<false, false, PREC, STREAM, PAGED, INTER><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  if constexpr (ORDER == 2) {
+    // the resident order serves span maps only
+    fused_kernel<false, false, PREC, STREAM, PAGED, 2><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  } else {
+    if (identity && ds128)
+      fused_kernel<true, true, PREC, STREAM, PAGED, ORDER><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+    else if (identity)
+      fused_kernel<true, false, PREC, STREAM, PAGED, ORDER><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+    else
+      fused_kernel<false, false, PREC, STREAM, PAGED, ORDER><<<dim3(grid), dim3(kThreads), 0, st>>>(a);
+  }
 }
 
-// tile order (interleaved or contiguous ranges) as a template argument
+// tile order (contiguous ranges, interleaved, or resident) as a template
+// argument; the host picks the resident order only for span maps with
+// several N tiles (cached source loads)
 template <int PREC, bool STREAM, bool PAGED>
 void launch_psp(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
-  if (a.interleave)
-    launch_pspi<PREC, STREAM, PAGED, true>(identity, ds128, grid, st, a);
-  else
-    launch_pspi<PREC, STREAM, PAGED, false>(identity, ds128, grid, st, a);
+  if (a.interleave == 1) {
+    launch_pspi<PREC, STREAM, PAGED, 1>(identity, ds128, grid, st, a);
+    return;
+  }
+  if constexpr (!STREAM) {
+    if (a.interleave == 2) {
+      launch_pspi<PREC, STREAM, PAGED, 2>(identity, ds128, grid, st, a);
+      return;
+    }
+  }
+  launch_pspi<PREC, STREAM, PAGED, 0>(identity, ds128, grid, st, a);
 }
 
 template <int PREC, bool STREAM>

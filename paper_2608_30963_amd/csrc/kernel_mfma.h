@@ -128,11 +128,19 @@ __device__ __forceinline__ void tile_context(int n_ctx, const CtxTable& cx, Tile
   T.tt = __builtin_amdgcn_readfirstlane(cx.t_tgt[b]);
   T.rb = __builtin_amdgcn_readfirstlane(cx.row_base[b]);
 }
-__device__ __forceinline__ Tile decode_tile(bool inter, int tau, int n_tiles, int row_tiles,
+__device__ __forceinline__ Tile decode_tile(int order, int tau, int n_tiles, int row_tiles,
                                             int n_ctx, const CtxTable& cx) {
   Tile T;
   T.tau = tau;
-  if (inter) {
+  if (order == 2) {
+    // resident: layer slowest, then row tile, then K|V, N tile fastest
+    T.nt = tau % n_tiles;
+    int rest = tau / n_tiles;
+    T.kv = rest & 1;
+    rest >>= 1;
+    T.rt = rest % row_tiles;
+    T.l = rest / row_tiles;
+  } else if (order == 1) {
     T.nt = tau % n_tiles;
     int rest = tau / n_tiles;
     T.rt = rest % row_tiles;
@@ -149,6 +157,24 @@ __device__ __forceinline__ Tile decode_tile(bool inter, int tau, int n_tiles, in
   }
   tile_context(n_ctx, cx, T);
   return T;
+}
+// The next tile of a contiguous range (resident order: N tile fastest, then
+// K|V, then row tile).
+__device__ __forceinline__ void advance_tile_res(int n_tiles, int row_tiles, int n_ctx,
+                                                 const CtxTable& cx, Tile& T) {
+  ++T.tau;
+  if (++T.nt < n_tiles) return;
+  T.nt = 0;
+  if (T.kv == 0) {
+    T.kv = 1;
+    return;
+  }
+  T.kv = 0;
+  if (++T.rt == row_tiles) {
+    T.rt = 0;
+    ++T.l;
+  }
+  tile_context(n_ctx, cx, T);
 }
 // The next tile of a contiguous range.
 __device__ __forceinline__ void advance_tile(int n_tiles, int row_tiles, int n_ctx,
@@ -233,6 +259,11 @@ __device__ __forceinline__ void st_stream(bf16_t* p, const uint4 v) {
   w.z = v.z;
   w.w = v.w;
   __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(p));
+}
+
+// Target row piece store of the span-map epilogue (paged layout).
+__device__ __forceinline__ void st_out(bf16_t* p, const u32x4 v) {
+  *reinterpret_cast<u32x4*>(p) = v;
 }
 
 // Round 8 floats to bf16 (hardware round-to-nearest-even) and pack.
@@ -394,12 +425,16 @@ __device__ __forceinline__ void store_rows(const FusedArgs& a, const Tile& Tc, c
 //
 // STREAM: source rows are read with streaming loads (one N tile, so no tile
 // re-reads them).  PAGED: target rows go through the block table.
-template <bool IDENT, bool CS_CACHE, int PREC, bool STREAM, bool PAGED, bool INTER>
+template <bool IDENT, bool CS_CACHE, int PREC, bool STREAM, bool PAGED, int ORDER>
 __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
-  // Row stores in the step after the staging (identity alignment), or in the
-  // epilogue step itself after a mid-step barrier (span maps: the pooling
-  // loop's dependent loads would otherwise wait behind the stores).
-  constexpr bool kDeferStores = IDENT;
+  // Identity alignment: the consumers stage a finished tile in LDS and the
+  // producers store its rows in the step after.  Span maps: the consumers
+  // store the rows straight from their accumulators (kDirect), so the LDS
+  // buffers hold only operands -- which lets the resident order (ORDER 2)
+  // keep a row tile's chunks in them for all of its N tiles.
+  constexpr bool kDirect = !IDENT;
+  constexpr bool RES = ORDER == 2;
+  static_assert(!RES || kDirect, "the resident order needs direct stores");
   __shared__ __attribute__((aligned(16))) bf16_t lds[fused_lds_bytes() / 2];
   // layer map and source RoPE frequencies: per-lane lookups go to LDS, so no
   // vector load inside the step loop can queue behind outstanding stores
@@ -418,7 +453,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   // contiguous piece per workgroup.  Interleaved order: it is dealt
   // round-robin, workgroup `slot` of the XCD taking tiles xbeg + slot,
   // xbeg + slot + nq, ...
-  constexpr bool inter = INTER;  // a.interleave, as a template argument
+  constexpr bool inter = ORDER == 1;  // a.interleave, as a template argument
   const int G = gridDim.x;
   const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
   const int nq = G / 8 + (xcd < G % 8 ? 1 : 0);          // workgroups on this XCD
@@ -446,13 +481,15 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   }
   const int n_tiles = a.n_tiles, row_tiles = a.row_tiles, n_ctx = a.ba.n;
   auto tile_at = [&](int tau) KVX_INLINE {
-    return decode_tile(inter, tau, n_tiles, row_tiles, n_ctx, ctx);
+    return decode_tile(ORDER, tau, n_tiles, row_tiles, n_ctx, ctx);
   };
   // the workgroup's next tile (called only while one remains)
   const int step_dn = nq % n_tiles, step_dr = nq / n_tiles;
   auto next_tile = [&](Tile& T) KVX_INLINE {
-    if (inter)
+    if constexpr (inter)
       step_tile(step_dn, step_dr, n_tiles, row_tiles, n_ctx, ctx, T);
+    else if constexpr (RES)
+      advance_tile_res(n_tiles, row_tiles, n_ctx, ctx, T);
     else
       advance_tile(n_tiles, row_tiles, n_ctx, ctx, T);
   };
@@ -515,15 +552,25 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     const int j0 = hp0 / a.hs, h0 = hp0 % a.hs, i00 = (8 * g) % half;
     // Position of a chunk: its tile, chunk index in the tile, this thread's
     // group; advanced one chunk at a time (no divisions in the step loop).
+    // ord: tile ordinal within this workgroup's range (resident order: of the
+    // first tile of the chunk's row-tile group in the range)
     struct ChunkPos {
       Tile T;
-      int c, j, h, i0, ord;  // ord: tile ordinal within this workgroup's range
+      int c, j, h, i0, ord;
     };
     auto advance_pos = [&](ChunkPos& P) KVX_INLINE {
       if (++P.c == nch) {
         P.c = 0;
-        ++P.ord;
-        if (P.ord < ntw) next_tile(P.T);
+        if constexpr (RES) {
+          // the next (layer, row tile, K|V) group: skip this group's other N tiles
+          const int k = n_tiles - P.T.nt;
+          P.ord += k;
+          if (P.ord < ntw)
+            for (int i = 0; i < k; ++i) next_tile(P.T);
+        } else {
+          ++P.ord;
+          if (P.ord < ntw) next_tile(P.T);
+        }
         P.j = j0;
         P.h = h0;
         P.i0 = i00;
@@ -542,6 +589,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       const int ls = lmap[P.T.l * a.mix + P.j];
       return a.src[P.T.kv] + ls * a.ss.l + P.T.b * a.ss.b + P.h * a.ss.h + P.i0;
     };
+    // chunks this workgroup's producers transform: one per chunk step, or, in
+    // the resident order, nch per row-tile group its range touches
+    const int nprod = RES ? (tile_at(tfirst).nt + ntw + n_tiles - 1) / n_tiles * nch : nchunks;
     ChunkPos fpos;
     fpos.T = tile_at(tfirst);
     fpos.c = 0;
@@ -768,14 +818,14 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     // chunk cs is consumed at step (its tile ordinal) * spt + (its index in the
     // tile) and written into that step's buffer during the step before.
     fetch_issue(fetch_addr(true), rA, true);
-    fetch_issue(fetch_addr(nchunks > 1), rB, nchunks > 1);
-    if constexpr (kDepth == 3) fetch_issue(fetch_addr(nchunks > 2), rC, nchunks > 2);
+    fetch_issue(fetch_addr(nprod > 1), rB, nprod > 1);
+    if constexpr (kDepth == 3) fetch_issue(fetch_addr(nprod > 2), rC, nprod > 2);
     {
-      const bf16_t* gp = fetch_addr(nchunks > kDepth);
+      const bf16_t* gp = fetch_addr(nprod > kDepth);
       second_issue(rA, true);
       transform(rA, lds, lds + kPlane);
-      second_issue(rB, nchunks > 1);
-      fetch_issue(gp, rA, nchunks > kDepth);
+      second_issue(rB, nprod > 1);
+      fetch_issue(gp, rA, nprod > kDepth);
     }
     lds_barrier();
     // Step s ends with a barrier; in an epilogue step (sc == nch) the
@@ -789,7 +839,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     Tile stT = tile_at(tfirst);
     int st_ord = 0;
     int32_t blk[kRowsPerThread];
-    load_blocks<PAGED>(a, stT, tid, blk);
+    if constexpr (!kDirect) load_blocks<PAGED>(a, stT, tid, blk);
     // Bias entry `tid` of a tile in staging-column order (consumer wave
     // tid / 64, block tid / 32 % 2, feature tid % 32); pair blocks past dout
     // read the zero sink.
@@ -819,10 +869,6 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     auto end_step = [&]() KVX_INLINE {
       if (sc == 0 && s > 0) biasl[sord & 1][tid] = bias_next;
       if (sc == nch) {
-        if (!kDeferStores) {
-          lds_barrier();  // staging complete
-          store_tile(s & 1);
-        }
         if (bias_ord + 1 < ntw) {
           next_tile(biasT);
           ++bias_ord;
@@ -835,39 +881,50 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         sc = 0;
         ++sord;
       }
-      // deferred: the tile staged in step s - 1, before this thread's
-      // transform of step s reuses the slots
-      if (kDeferStores && sc == 0) store_tile((s - 1) & 1);
+      // identity alignment: the tile staged in step s - 1, before this
+      // thread's transform of step s reuses the slots
+      if constexpr (!kDirect)
+        if (sc == 0) store_tile((s - 1) & 1);
     };
-    // Transform the next chunk (the one at tpos, consumed at step
-    // tpos.ord * spt + tpos.c) during the step before it, from raw set R, and
+    // Step in which the chunk at P is written: the step before its first use
+    // (step ord * spt + c, buffer s % 2) -- or, in the resident order, where
+    // chunk c of a group lives in buffer c, the step after the previous
+    // group's last use of buffer c.
+    auto write_step = [&](const ChunkPos& P) KVX_INLINE -> int {
+      if constexpr (RES)
+        return P.ord == 0 ? P.c - 1 : (P.ord - 1) * spt + P.c + 1;
+      else
+        return P.ord * spt + P.c - 1;
+    };
+    // Transform the next chunk (the one at tpos, written at write_step) from
+    // raw set R, and
     // refill R with the chunk kDepth further on.  Called with the sets in turn
     // (chunk mod kDepth), so each set keeps its registers.
     auto produce = [&](int next, Raw& R, const Raw& Rn) KVX_INLINE {
-      while (s + 1 < tpos.ord * spt + tpos.c) end_step();  // steps with nothing to transform
-      bf16_t* buf = lds + ((s + 1) & 1) * 2 * kPlane;
-      const bool more = next + kDepth < nchunks;
+      while (s < write_step(tpos)) end_step();  // steps with nothing to transform
+      bf16_t* buf = lds + (RES ? tpos.c : (s + 1) & 1) * 2 * kPlane;
+      const bool more = next + kDepth < nprod;
       const bf16_t* gp = fetch_addr(more);
       transform(R, buf, buf + kPlane);
-      second_issue(Rn, next + 1 < nchunks);  // Rn: the chunk after this one
+      second_issue(Rn, next + 1 < nprod);  // Rn: the chunk after this one
       fetch_issue(gp, R, more);
       end_step();
     };
     int next = 1;
     if constexpr (kDepth == 3) {
-      for (; next + 2 < nchunks; next += 3) {
+      for (; next + 2 < nprod; next += 3) {
         produce(next, rB, rC);
         produce(next + 1, rC, rA);
         produce(next + 2, rA, rB);
       }
-      if (next < nchunks) produce(next, rB, rC);
-      if (next + 1 < nchunks) produce(next + 1, rC, rA);
+      if (next < nprod) produce(next, rB, rC);
+      if (next + 1 < nprod) produce(next + 1, rC, rA);
     } else {
-      for (; next + 1 < nchunks; next += 2) {
+      for (; next + 1 < nprod; next += 2) {
         produce(next, rB, rA);
         produce(next + 1, rA, rB);
       }
-      if (next < nchunks) produce(next, rB, rA);
+      if (next < nprod) produce(next, rB, rA);
     }
     while (s < nsteps) end_step();
     return;
@@ -983,20 +1040,147 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     }
   };
 
+  // Span maps (kDirect): the epilogue of a tile -- bias, target RoPE on K,
+  // bf16 -- with the rows stored straight from the accumulators.  A lane holds, for token column lane%32 of
+  // token block m, the features 8*(v/4) + 4*(lane/32) + v%4 (v < 16) of
+  // blocks c0 and c1.  For each pair of 8-feature groups (g4 = 2gp, 2gp+1),
+  // v_permlane32_swap gives lane l the upper half of group 2gp from lane
+  // l + 32 and lane l + 32 the lower half of group 2gp+1 from lane l, so each
+  // lane then holds one 16-byte piece (8 consecutive features) of its row and
+  // the two lanes of a row store adjacent pieces.  Bias comes from the tile's
+  // LDS copy; the RoPE angle is formed in fp64 for token block 0 and advanced
+  // by 32 positions per block with the rotation by 32 positions.  Lanes past
+  // the context's end, and pair blocks past dout, store to the trash area, so
+  // the stores stay unconditional.
+  // Feature groups 2gp and 2gp + 1 of every token block (gp = 0, 1).
+  auto finish = [&](const Tile& Tc, const Blocks& B, const float* bias_t,
+                    const int32_t (&blk)[4], const int gp) KVX_INLINE {
+    const bool is_k = Tc.kv == 0;
+    const int half = lane / 32;
+    const float* bl = bias_t + cw * 64 + fq;
+    bf16_t* dst = a.tgt[Tc.kv] + Tc.l * a.ts.l + static_cast<int64_t>(B.hp) * a.ts.h;
+    const int col = 32 * B.q + 8 * (2 * gp + half);
+    // Contiguous layout: this context's rows of the head as a buffer resource
+    // whose size ends at row T_t (zero for a pair block past dout), so the
+    // hardware drops the stores of rows past the context's end; offsets are
+    // 32-bit (the host keeps a context's rows below 2^31 bytes).
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        dst + (PAGED ? 0 : static_cast<int64_t>(Tc.b) * a.ts.b), static_cast<short>(0),
+        B.on && !PAGED ? static_cast<int>(static_cast<int64_t>(Tc.tt) * a.ts.t * 2) : 0,
+        0x00020000);
+    // packed bf16 pairs of group 2gp, [token block][block c0|c1][dword]
+    uint32_t w0[4][2][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int g4 = 2 * gp + h;
+      const f32x4 b0 = *reinterpret_cast<const f32x4*>(bl + 8 * g4);
+      const f32x4 b1 = *reinterpret_cast<const f32x4*>(bl + 32 + 8 * g4);
+      float cs[4], sn[4], c32[4], s32[4];
+      if (is_k) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int fi = 32 * B.q + 8 * g4 + fq + i;
+          rope_cs(ftl[fi], Tc.t0 + lane % 32, cs[i], sn[i]);
+          const float2 r = rot32[fi];
+          c32[i] = r.x;
+          s32[i] = r.y;
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        float u0[4], u1[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          u0[i] = acc[m][0][4 * g4 + i] + b0[i];
+          u1[i] = acc[m][1][4 * g4 + i] + b1[i];
+        }
+        if (is_k) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float y0 = u0[i] * cs[i] - u1[i] * sn[i];
+            const float y1 = u1[i] * cs[i] + u0[i] * sn[i];
+            u0[i] = y0;
+            u1[i] = y1;
+            // angle of token block m + 1
+            const float c2 = cs[i] * c32[i] - sn[i] * s32[i];
+            sn[i] = sn[i] * c32[i] + cs[i] * s32[i];
+            cs[i] = c2;
+          }
+        }
+        uint32_t q[2][2];  // [block c0|c1][dword]
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+          const bf16x2 q0 = {static_cast<__bf16>(u0[2 * d]), static_cast<__bf16>(u0[2 * d + 1])};
+          const bf16x2 q1 = {static_cast<__bf16>(u1[2 * d]), static_cast<__bf16>(u1[2 * d + 1])};
+          q[0][d] = __builtin_bit_cast(uint32_t, q0);
+          q[1][d] = __builtin_bit_cast(uint32_t, q1);
+        }
+        if (h == 0) {
+#pragma unroll
+          for (int p = 0; p < 2; ++p)
+#pragma unroll
+            for (int d = 0; d < 2; ++d) w0[m][p][d] = q[p][d];
+          continue;
+        }
+        // trade halves with the partner lane, then store one piece per block
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+          for (int d = 0; d < 2; ++d) {
+            const auto r = __builtin_amdgcn_permlane32_swap(w0[m][p][d], q[p][d], false, false);
+            w0[m][p][d] = r[0];
+            q[p][d] = r[1];
+          }
+        const int t = Tc.t0 + m * 32 + lane % 32;
+        const u32x4 v0 = {w0[m][0][0], w0[m][0][1], q[0][0], q[0][1]};
+        const u32x4 v1 = {w0[m][1][0], w0[m][1][1], q[1][0], q[1][1]};
+        if constexpr (PAGED) {
+          const int64_t row = static_cast<int64_t>(blk[m]) * a.ts.b +
+                              static_cast<int64_t>(t % a.pg.block_size) * a.ts.t;
+          const bool ok = t < Tc.tt && B.on;
+          st_out(ok ? dst + row + col : a.trash, v0);
+          st_out(ok ? dst + row + col + a.dt / 2 : a.trash, v1);
+        } else {
+          const int off = (t * static_cast<int>(a.ts.t) + col) * 2;
+          __builtin_amdgcn_raw_buffer_store_b128(v0, rs, off, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(v1, rs, off + a.dt, 0, 0);
+        }
+      }
+    }
+  };
+  // Physical blocks of this lane's rows (token lane%32 of each token block)
+  // of tile Tc, loaded when the consumers start the tile (unconditional
+  // loads: rows past the context's end read the last row's entry).
+  auto tile_blocks = [&](const Tile& Tc, int32_t (&blk)[4]) KVX_INLINE {
+    if constexpr (PAGED) {
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int t = Tc.t0 + m * 32 + lane % 32;
+        const int tc = t < Tc.tt ? t : Tc.tt - 1;
+        blk[m] = a.pg.table[Tc.b * a.pg.max_blocks + tc / a.pg.block_size];
+      }
+    }
+  };
+
   Tile T = tile_at(tfirst);
   Blocks B = blocks(T, cw);
   Tile Tn = T;      // next tile (decoded in the step that loads its weights)
   Blocks Bn = B;
+  int32_t cblk[4] = {0, 0, 0, 0};  // paged span maps: blocks of this lane's rows of T
   load_w(B, 0);  // valid addresses even for a pair block past dout
   lds_barrier();
   int cs = 0;    // global chunk index
   int c = 0;     // chunk within the tile; c == nch: epilogue step
   int tpar = 0;  // tile parity (bias buffer)
   for (int s = 0; s < nsteps; ++s) {
-    bf16_t* buf = lds + (s & 1) * 2 * kPlane;
+    // resident order: chunk c of a row-tile group stays in buffer c for all of
+    // the group's N tiles
+    bf16_t* buf = lds + (RES ? c : s & 1) * 2 * kPlane;
     if (c < nch) {
       // ---------------- chunk step ----------------
       const bool computed = T.kv == 0 || !IDENT;
+      if constexpr (kDirect && PAGED)
+        if (c == 0) tile_blocks(T, cblk);
       // k-steps of this chunk that take the split operand (a uniform load)
       const int kmask =
           PREC == kBF16X2 && a.split_mask ? a.split_mask[(T.l * 2 + T.kv) * nch + c] : 0xFF;
@@ -1091,9 +1275,13 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       lds_barrier();
     } else {
       // ---------------- epilogue step ----------------
-      if (B.on) stage(T, B, buf, biasl[tpar]);
-      lds_barrier();  // staging complete
-      if (!kDeferStores) lds_barrier();  // the producers' row stores
+      if constexpr (kDirect) {
+        finish(T, B, biasl[tpar], cblk, 0);
+        finish(T, B, biasl[tpar], cblk, 1);
+      } else {
+        if (B.on) stage(T, B, buf, biasl[tpar]);
+      }
+      lds_barrier();
       if (cs < nchunks) {
         T = Tn;
         B = Bn;

@@ -63,10 +63,13 @@ struct kvx_plan {
   void* trash = nullptr;
   uint8_t* split_mask = nullptr; // precision BF16X2_OUTLIER: [Lt][2][din/128]
   int64_t split_ksteps = 0, ksteps = 0;
-  // fused kernel: interleaved tile order when one tile's weight slice
+  // fused kernel: interleaved tile order (1) when one tile's weight slice
   // (din x 256 bf16) reaches 512 KiB; with contiguous ranges the workgroups
   // of an XCD would then keep several layers' translators in flight, more
-  // than its 4 MiB L2 holds
+  // than its 4 MiB L2 holds.  Resident order (2) when a row tile's whole
+  // contraction (din <= 256) fits the kernel's two LDS buffers and the
+  // output has several N tiles: the chunks are transformed once and kept
+  // for all N tiles (span maps; identity-aligned calls use 0).
   int32_t tile_order = 0;
   void* block = nullptr;         // single allocation backing all of the above
 };
@@ -181,7 +184,7 @@ kvx_status kvx_plan_create(const kvx_plan_desc* d, kvx_plan** out) {
     delete p;
     return KVX_EUNSUPPORTED;
   }
-  p->tile_order = p->kernel == kFused && p->din >= 1024 ? 1 : 0;
+  p->tile_order = p->kernel != kFused ? 0 : p->din >= 1024 ? 1 : (p->din <= 256 && p->dout > 256) ? 2 : 0;
 
   auto fail = [&](kvx_status s) {
     kvx_plan_destroy(p);
@@ -487,6 +490,10 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
         !aligned16(io.tgt_v))
       fused = false;
   }
+  // the fused kernel addresses a context's rows of one head with 32-bit byte
+  // offsets (contiguous layout)
+  if (fused && !paged && int64_t(io.tgt_capacity) * io.tgt_stride[3] * esz > INT32_MAX)
+    fused = false;
   if (p->kernel == kFused && !fused) return KVX_EUNSUPPORTED;
 
   const Strides ss{io.src_stride[0], io.src_stride[1], io.src_stride[2], io.src_stride[3]};
@@ -553,7 +560,10 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
       const int64_t total = int64_t(tiles) * a.n_tiles * 2 * Lt;
       if (total > INT32_MAX) return KVX_ESHAPE;
       a.total_tiles = static_cast<int32_t>(total);
-      a.interleave = p->tile_order;
+      // the resident order (a row tile's chunks kept in LDS for its N tiles)
+      // serves span maps; identity-aligned calls of such plans take the
+      // contiguous order
+      a.interleave = p->tile_order == 2 && identity ? 0 : p->tile_order;
       // persistent: one workgroup per compute unit (the kernel's LDS use
       // allows exactly one)
       const int grid = static_cast<int>(total < p->n_cu ? total : p->n_cu);

@@ -136,6 +136,29 @@ def test_interleaved_tile_order():
     _check(short, expect_order=0)
 
 
+def test_resident_order_shapes():
+    """The resident order (span maps, din <= 256, several N tiles): a single
+    K-chunk (din 128) with a partly used second N tile, two chunks with
+    three N tiles over more row-tile groups than compute units (so that
+    workgroup ranges begin and end inside groups), and ragged contexts."""
+    one = _spec(name="resident-1chunk", src=S.ModelShape(2, 1, 128, 1.0e6),
+                tgt=S.ModelShape(2, 3, 128, 1.0e4), layer_map=(1, 0), src_tokens=700, batch=3,
+                span_lo=1, span_hi=3)
+    _check(S.make_problem(one), expect_order=2)
+    _check(S.make_problem(one), precision=kvx.KVX_PREC_F16, expect_order=2)
+    two = _spec(name="resident-groups", src=S.ModelShape(3, 2, 128, 1.0e6),
+                tgt=S.ModelShape(2, 6, 128, 1.0e4), layer_map=(2, 0), src_tokens=2000,
+                batch=9, span_lo=1, span_hi=2)
+    prob = S.make_problem(two)
+    n_cu = U.torch().cuda.get_device_properties(0).multi_processor_count
+    groups = sum(-(-int(t) // 128) for t in prob.tgt_tokens) * 2 * 2
+    assert groups > n_cu, (groups, n_cu)
+    _check(prob, expect_order=2)
+    # identity alignment on such a plan takes the contiguous order
+    _check(S.make_problem(dataclasses.replace(two, name="resident-plan-identity", span_lo=0,
+                                              span_hi=0, batch=2, src_tokens=300)))
+
+
 def test_strided_source_view():
     """Source K/V are views into larger caches (extra tokens after T_s)."""
     T = U.torch()

@@ -89,7 +89,10 @@ def test_paged_config2_flash_layout_f16():
 
 
 def test_paged_config3_span_map_batch():
-    _run_paged(S.config(3, src_tokens=700, batch=2), block_size=32)
+    """Span map with several N tiles: the resident order, rows stored through
+    the block table from the consumers; also the flash-style layout."""
+    _run_paged(S.config(3, src_tokens=700, batch=2), block_size=32, expect_order=2)
+    _run_paged(S.config(3, src_tokens=500, batch=3), block_size=16, flash=True, expect_order=2)
 
 
 def test_paged_config5_interleaved_span_map():
