@@ -941,28 +941,29 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   const int tcol = 8 * (lane / 32);
   const int fq = 4 * (lane / 32);
 
+  // The consumer wave's pair block of a tile, kept compact (registers are
+  // scarce): its index pb = 4 nt + wave and the weight fragment pointer of
+  // its first 32 features c0 = hp Dt + 32 q (target head hp, block q of the
+  // head); the RoPE partners c1 = c0 + Dt/2 lie w1off fragments further.  A
+  // pair block past dout (on() false) points at block 0 and stores nothing.
   struct Blocks {
-    int on, nt;
-    int c0, c1, q, hp;
+    int pb;
     const bf16x8* w0p;
-    const bf16x8* w1p;
   };
-  // weight fragment pointers of blocks c0 / c1 for tile T's layer and K|V
+  auto b_on = [&](const Blocks& B) KVX_INLINE { return B.pb < npb; };
+  auto b_hp = [&](const Blocks& B) KVX_INLINE { return B.pb < npb ? B.pb / per_head : 0; };
+  auto b_q = [&](const Blocks& B) KVX_INLINE { return B.pb < npb ? B.pb % per_head : 0; };
+  const int64_t w1off = static_cast<int64_t>(a.dt / 64) * KSALL * 64;
+  // weight fragment pointer of block c0 for tile T's layer and K|V
   auto rebase = [&](Blocks& B, const Tile& T) KVX_INLINE {
     const bf16x8* wsel = PREC == kF16 ? a.wh[T.kv] : a.wp[T.kv];
     const bf16x8* base = wsel + static_cast<int64_t>(T.l) * (a.dout / 32) * KSALL * 64;
-    B.w0p = base + static_cast<int64_t>(B.c0 / 32) * KSALL * 64 + lane;
-    B.w1p = base + static_cast<int64_t>(B.c1 / 32) * KSALL * 64 + lane;
+    const int c0 = b_hp(B) * a.dt + 32 * b_q(B);
+    B.w0p = base + static_cast<int64_t>(c0 / 32) * KSALL * 64 + lane;
   };
   auto blocks = [&](const Tile& T, int w) KVX_INLINE {
     Blocks B;
-    const int pb = T.nt * 4 + w;
-    B.nt = T.nt;
-    B.on = pb < npb;
-    B.hp = B.on ? pb / per_head : 0;
-    B.q = B.on ? pb % per_head : 0;
-    B.c0 = B.hp * a.dt + 32 * B.q;
-    B.c1 = B.c0 + a.dt / 2;
+    B.pb = T.nt * 4 + w;
     rebase(B, T);
     return B;
   };
@@ -974,7 +975,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       wf[ks][0] = B.w0p[(c * 8 + ks) * 64];
-      wf[ks][1] = B.w1p[(c * 8 + ks) * 64];
+      wf[ks][1] = B.w0p[w1off + (c * 8 + ks) * 64];
     }
   };
 
@@ -995,7 +996,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       if (is_k) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int fi = 32 * B.q + 8 * g4 + fq + i;
+          const int fi = 32 * b_q(B) + 8 * g4 + fq + i;
           rope_cs(ftl[fi], Tc.t0 + lane % 32, cs[i], sn[i]);
           const float2 r = rot32[fi];
           c32[i] = r.x;
@@ -1058,15 +1059,15 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
     const bool is_k = Tc.kv == 0;
     const int half = lane / 32;
     const float* bl = bias_t + cw * 64 + fq;
-    bf16_t* dst = a.tgt[Tc.kv] + Tc.l * a.ts.l + static_cast<int64_t>(B.hp) * a.ts.h;
-    const int col = 32 * B.q + 8 * (2 * gp + half);
+    bf16_t* dst = a.tgt[Tc.kv] + Tc.l * a.ts.l + static_cast<int64_t>(b_hp(B)) * a.ts.h;
+    const int col = 32 * b_q(B) + 8 * (2 * gp + half);
     // Contiguous layout: this context's rows of the head as a buffer resource
     // whose size ends at row T_t (zero for a pair block past dout), so the
     // hardware drops the stores of rows past the context's end; offsets are
     // 32-bit (the host keeps a context's rows below 2^31 bytes).
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         dst + (PAGED ? 0 : static_cast<int64_t>(Tc.b) * a.ts.b), static_cast<short>(0),
-        B.on && !PAGED ? static_cast<int>(static_cast<int64_t>(Tc.tt) * a.ts.t * 2) : 0,
+        b_on(B) && !PAGED ? static_cast<int>(static_cast<int64_t>(Tc.tt) * a.ts.t * 2) : 0,
         0x00020000);
     // packed bf16 pairs of group 2gp, [token block][block c0|c1][dword]
     uint32_t w0[4][2][2];
@@ -1079,7 +1080,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       if (is_k) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int fi = 32 * B.q + 8 * g4 + fq + i;
+          const int fi = 32 * b_q(B) + 8 * g4 + fq + i;
           rope_cs(ftl[fi], Tc.t0 + lane % 32, cs[i], sn[i]);
           const float2 r = rot32[fi];
           c32[i] = r.x;
@@ -1137,7 +1138,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         if constexpr (PAGED) {
           const int64_t row = static_cast<int64_t>(blk[m]) * a.ts.b +
                               static_cast<int64_t>(t % a.pg.block_size) * a.ts.t;
-          const bool ok = t < Tc.tt && B.on;
+          const bool ok = t < Tc.tt && b_on(B);
           st_out(ok ? dst + row + col : a.trash, v0);
           st_out(ok ? dst + row + col + a.dt / 2 : a.trash, v1);
         } else {
@@ -1193,7 +1194,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       if (more && cn == 0) {
         Tn = T;
         next_tile(Tn);
-        if (Tn.nt == B.nt) {
+        if (Tn.nt == (B.pb >> 2)) {
           Bn = B;
           rebase(Bn, Tn);
         } else {
@@ -1203,16 +1204,20 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       // unconditional (past the last chunk, or for a pair block past dout, the
       // addresses are still valid fragments): the compiler then counts the
       // outstanding loads exactly instead of draining them all
+      // (span maps: the last chunk of a tile leaves k-steps 0..3 of the next
+      // tile to the end of the epilogue, whose direct stores need the
+      // registers)
+      const bool hold = false;
       auto reload = [&](int ks) KVX_INLINE {
         if (ks < 4) {
           wf[ks][0] = B.w0p[(c * 8 + ks + 4) * 64];
-          wf[ks][1] = B.w1p[(c * 8 + ks + 4) * 64];
-        } else {
+          wf[ks][1] = B.w0p[w1off + (c * 8 + ks + 4) * 64];
+        } else if (!hold) {
           wf[ks - 4][0] = Bn.w0p[(cn * 8 + ks - 4) * 64];
-          wf[ks - 4][1] = Bn.w1p[(cn * 8 + ks - 4) * 64];
+          wf[ks - 4][1] = Bn.w0p[w1off + (cn * 8 + ks - 4) * 64];
         }
       };
-      if (B.on) {
+      if (b_on(B)) {
         const bf16_t* hi = buf;
         const bf16_t* lo = buf + kPlane;
         // MFMA groups run in the order (k-step, plane): the token fragments of
@@ -1267,7 +1272,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
           reload(ks);
           __builtin_amdgcn_sched_barrier(0);
         }
-      } else {
+      } else if (!hold) {
         load_w(Bn, cn);
       }
       ++cs;
@@ -1279,7 +1284,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
         finish(T, B, biasl[tpar], cblk, 0);
         finish(T, B, biasl[tpar], cblk, 1);
       } else {
-        if (B.on) stage(T, B, buf, biasl[tpar]);
+        if (b_on(B)) stage(T, B, buf, biasl[tpar]);
       }
       lds_barrier();
       if (cs < nchunks) {
