@@ -93,6 +93,8 @@ constexpr int kSinkBytes = 2048;
 constexpr int fused_lds_bytes() { return 2 * 2 * kPlane * 2; }
 constexpr int kMaxLayerMap = 1024;  // target layers * mix held in LDS
 constexpr int kMaxHalfDim = 256;    // source head_dim / 2 held in LDS
+constexpr int kDTab = 3;            // relative source rotations held in LDS: |d| <= 3
+constexpr int kTabHalf = 64;        // ... for source head_dim <= 128
 
 struct Tile {
   int l, kv, nt, b, t0, tt, rb, rt;
@@ -440,6 +442,9 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
   // vector load inside the step loop can queue behind outstanding stores
   __shared__ int32_t lmap[kMaxLayerMap];
   __shared__ double fsl[kMaxHalfDim];
+  // span maps: cos / sin of the source rotation by d = -kDTab .. kDTab
+  // positions, [d + kDTab][i] for i < kTabHalf (source head_dim <= 128)
+  __shared__ float2 rotd[(2 * kDTab + 1) * kTabHalf];
   // target RoPE: theta_i / 2pi, and cos/sin of the rotation by 32 positions
   __shared__ double ftl[kMaxHalfDim];
   __shared__ float2 rot32[kMaxHalfDim];
@@ -494,6 +499,14 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       advance_tile(n_tiles, row_tiles, n_ctx, ctx, T);
   };
   for (int i = tid; i < a.ds / 2; i += kThreads) fsl[i] = a.fs[i];
+  const bool dtab = a.ds <= 2 * kTabHalf;
+  if constexpr (!IDENT) {
+    for (int i = tid; i < (2 * kDTab + 1) * kTabHalf; i += kThreads) {
+      float c = 1.f, sn = 0.f;
+      if (i % kTabHalf < a.ds / 2) rope_cs(a.fs[i % kTabHalf], i / kTabHalf - kDTab, c, sn);
+      rotd[i] = make_float2(c, sn);
+    }
+  }
   for (int i = tid; i < a.dt / 2; i += kThreads) {
     ftl[i] = a.ft[i];
     float c, sn;
@@ -728,7 +741,49 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
       for (int u = 0; u < kUnits; ++u) {
         const int r = tid / 8 + 32 * u;
         float z0[8], z1[8];
-        {
+        if constexpr (kPrefetch2) {
+          // First two entries.  For K they are pooled in the first entry's
+          // frame, R(-k0) (w0 x_k0 + w1 R(-(k1 - k0)) x_k1) -- equal to
+          // w0 R(-k0) x_k0 + w1 R(-k1) x_k1 -- so only the first entry needs
+          // a fresh fp64-reduced angle: the relative rotation of a nearby
+          // second token (|k1 - k0| <= kDTab, as in spans) comes from the
+          // rotd table; a farther one is formed like any other angle.  A row
+          // without a second entry has zero data and weight (and d = 0).
+          const int k0 = R.ri.k0[u];
+          const float w0 = R.ri.w0[u], w1 = ybw[u];
+          float x0[8], x1[8], v0[8], v1[8];
+          unpack8(R.x0[u], x0);
+          unpack8(R.x1[u], x1);
+          unpack8(yb0[u], v0);
+          unpack8(yb1[u], v1);
+          if (is_k) {
+            const int d = R.ri.e1[u] - R.ri.e0[u] >= 2 ? ybk[u] - k0 : 0;
+            const bool tab = dtab && d >= -kDTab && d <= kDTab;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              float cd, sd;
+              if (tab) {
+                const float2 t = rotd[(d + kDTab) * kTabHalf + pg.i0 + i];
+                cd = t.x;
+                sd = t.y;
+              } else {
+                rope_cs(f[i], d, cd, sd);
+              }
+              const float y0 = w0 * x0[i] + w1 * (v0[i] * cd + v1[i] * sd);
+              const float y1 = w0 * x1[i] + w1 * (v1[i] * cd - v0[i] * sd);
+              float cs_, sn;
+              rope_cs(f[i], k0, cs_, sn);
+              z0[i] = y0 * cs_ + y1 * sn;
+              z1[i] = y1 * cs_ - y0 * sn;
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              z0[i] = w0 * x0[i] + w1 * v0[i];
+              z1[i] = w0 * x1[i] + w1 * v1[i];
+            }
+          }
+        } else {
           float x0[8], x1[8];
           unpack8(R.x0[u], x0);
           unpack8(R.x1[u], x1);
@@ -750,27 +805,6 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(FusedArgs a) {
             }
             z0[i] = w * y0;
             z1[i] = w * y1;
-          }
-        }
-        if constexpr (kPrefetch2) {
-          // second entry, requested a step earlier (second_issue); zeros and
-          // a zero weight when absent
-          const int k = ybk[u];
-          const float w = ybw[u];
-          float x0[8], x1[8];
-          unpack8(yb0[u], x0);
-          unpack8(yb1[u], x1);
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            float v0 = x0[i], v1 = x1[i];
-            if (is_k) {
-              float cs_, sn;
-              rope_cs(f[i], k, cs_, sn);
-              v0 = x0[i] * cs_ + x1[i] * sn;
-              v1 = x1[i] * cs_ - x0[i] * sn;
-            }
-            z0[i] += w * v0;
-            z1[i] += w * v1;
           }
         }
         if constexpr (!IDENT) {
