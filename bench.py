@@ -78,12 +78,14 @@ def kernel_source_hash() -> str:
 PROFILES = os.path.join(ROOT, "profiles")
 
 
-def recorded_traffic(workload: str, precision: str, src_tokens: int, batch: int, layout: str,
-                     profiles: str = None):
-    """HBM bytes per launch from the committed rocprofv3 counter summary of
-    this workload (FETCH_SIZE and WRITE_SIZE, scaled by a copy kernel's
-    reading), or None when no summary matches or the kernel sources have
-    changed since the counters were taken."""
+def recorded(workload: str, precision: str, src_tokens: int, batch: int, layout: str,
+             key: str, profiles: str = None):
+    """A value recorded in the committed rocprofv3 counter summary of this
+    workload (profiles/*.md, "- key: value" lines), or None when no summary
+    matches or the kernel sources have changed since the counters were
+    taken: traffic_bytes_per_launch (FETCH_SIZE + WRITE_SIZE, scaled by a
+    copy kernel's reading), mfma_busy_frac (SQ_VALU_MFMA_BUSY_CYCLES per SIMD
+    over SQ_BUSY_CYCLES per shader engine)."""
     want = {"workload": workload, "precision": precision, "src_tokens": str(src_tokens),
             "batch": str(batch), "target_layout": layout,
             "kernel_source_sha256": kernel_source_hash()}
@@ -94,9 +96,17 @@ def recorded_traffic(workload: str, precision: str, src_tokens: int, batch: int,
                 if line.startswith("- ") and ": " in line:
                     k, v = line[2:].strip().split(": ", 1)
                     rec[k.strip("`")] = v.strip().strip("`")
-        if all(rec.get(k) == v for k, v in want.items()) and "traffic_bytes_per_launch" in rec:
-            return int(rec["traffic_bytes_per_launch"])
+        if all(rec.get(k) == v for k, v in want.items()) and key in rec:
+            return rec[key]
     return None
+
+
+def recorded_traffic(workload: str, precision: str, src_tokens: int, batch: int, layout: str,
+                     profiles: str = None):
+    """HBM bytes per launch (see recorded), or None."""
+    v = recorded(workload, precision, src_tokens, batch, layout, "traffic_bytes_per_launch",
+                 profiles)
+    return None if v is None else int(v)
 
 
 def cpu_baseline(spec, prob, budget_s: float):
@@ -182,6 +192,15 @@ def main():
     print(f"[bench] generating {spec.name} T={spec.src_tokens} B={spec.batch}",
           file=sys.stderr, flush=True)
     prob = S.make_problem(spec)
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib << 20
+        csrc = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        cdst = torch.empty_like(csrc)
+        torch.cuda.synchronize()
+        for _ in range(3):  # an elementwise kernel: reads n bytes, writes n bytes
+            torch.bitwise_not(csrc, out=cdst)
+        torch.cuda.synchronize()
+        del csrc, cdst
     if args.fit:
         return main_fit(args, spec, prob, torch, kvx, S)
     alg = algorithmic(spec, prob)
@@ -241,16 +260,6 @@ def main():
 
     def step(i):
         kvx.kvx_translate(tr.plan, ios[i % len(ios)][0], stream)
-
-    if args.calibrate_copy_mib > 0:
-        n = args.calibrate_copy_mib << 20
-        csrc = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
-        cdst = torch.empty_like(csrc)
-        torch.cuda.synchronize()
-        for _ in range(3):  # an elementwise kernel: reads n bytes, writes n bytes
-            torch.bitwise_not(csrc, out=cdst)
-        torch.cuda.synchronize()
-        del csrc, cdst
 
     # Clock settling: the GPU raises its clocks only after some time under
     # load (a 50-step run measured right after 5 warm-up calls is ~20% slower
@@ -318,11 +327,17 @@ def main():
     kernel_name = "fused_kernel" if info.kernel == 1 else "tiled_kernel"
     layout = f"paged, {args.paged}-token blocks" if args.paged else "contiguous"
     traffic = recorded_traffic(spec.name, args.precision, spec.src_tokens, spec.batch, layout)
+    busy = recorded(spec.name, args.precision, spec.src_tokens, spec.batch, layout,
+                    "mfma_busy_frac")
     roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kernel_name,
             "bytes_per_launch": alg["bytes"], "ms_per_launch": round(ms_kernel, 5),
             "mfma_tflops": round(tfs, 1),
-            "mfma_frac": round(tfs / MFMA_BF16_PEAK_TFS, 4)}
+            "mfma_frac": round(tfs / MFMA_BF16_PEAK_TFS, 4),
+            # counter-based: share of the kernel's cycles its SIMDs' matrix
+            # cores were busy (split operands issue more MFMAs than the
+            # algorithmic contraction counts), from the committed summary
+            "mfma_busy_frac": None if busy is None else float(busy)}
 
     cpu = None
     if not args.no_cpu and args.cpu_budget > 0:
