@@ -167,6 +167,9 @@ def main():
     ap.add_argument("--fit", action="store_true",
                     help="measure the translator fit (accumulate + solve) instead")
     ap.add_argument("--lam", type=float, default=1.0, help="ridge of the fit's solve")
+    ap.add_argument("--staged", action="store_true",
+                    help="measure the staged (three-launch) translation stage by stage, "
+                         "beside the fused kernel, instead")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="first run a plain device copy (bitwise_not) of this many MiB "
                          "(three times), "
@@ -203,6 +206,8 @@ def main():
         del csrc, cdst
     if args.fit:
         return main_fit(args, spec, prob, torch, kvx, S)
+    if args.staged:
+        return main_staged(args, spec, prob, torch, kvx, S)
     alg = algorithmic(spec, prob)
 
     def dev(a, f32=False):
@@ -364,6 +369,131 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+    tr.close()
+
+
+def staged_bytes(spec, prob, prec_split: bool):
+    """Bytes each launch of the staged translation moves (one pass over all
+    target layers): the algorithmic source, map, weight and target bytes of
+    the operator, plus the intermediates as the stages write and read them
+    (Z: bf16 planes, rows rounded up to 128 per context; U: fp32)."""
+    alg = algorithmic(spec, prob)
+    lt, din, dout = spec.tgt.n_layers, spec.d_in, spec.d_out
+    rows_p = int(sum((int(t) + 127) // 128 * 128 for t in prob.tgt_tokens))
+    ident = prob.row_ptr is None
+    planes = [2 if prec_split else 1, 2 if prec_split and not ident else 1]
+    z = sum(lt * p * rows_p * din * 2 for p in planes)
+    u = 2 * lt * rows_p * dout * 4
+    bias = 2 * lt * dout * 4
+    return {"pool": alg["read"] + alg["map"] + z, "project": z + alg["weights"] + u,
+            "store": u + bias + alg["write"], "z": z, "u": u,
+            "flops_issued": 2 * lt * rows_p * din * dout * sum(planes)}
+
+
+def main_staged(args, spec, prob, torch, kvx, S):
+    """Per-stage time and memory throughput of kvx_translate_staged (pool,
+    project, store: one launch each over all target layers), with the fused
+    kernel timed on the same buffers for comparison."""
+    if spec.dtype != "bf16" or args.paged:
+        print("bench.py --staged: bf16 workloads, contiguous target layout", file=sys.stderr)
+        sys.exit(2)
+    prec = {"bf16x2": kvx.KVX_PREC_BF16X2, "bf16": kvx.KVX_PREC_BF16}.get(args.precision)
+    if prec is None:
+        print("bench.py --staged: precision bf16x2 or bf16", file=sys.stderr)
+        sys.exit(2)
+
+    def dev(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    tr = kvx.Translator(spec.src, spec.tgt, spec.mix, spec.layer_map, kvx.KVX_BF16,
+                        dev(prob.w_k), dev(prob.w_v), dev(prob.b_k), dev(prob.b_v), prec)
+    ident = prob.row_ptr is None
+    rp, ci, wt = (None, None, None) if ident else (dev(prob.row_ptr), dev(prob.col_idx),
+                                                  dev(prob.weight))
+    cap = prob.tgt_capacity
+    oshape = (spec.tgt.n_layers, spec.batch, spec.tgt.n_kv_heads, cap, spec.tgt.head_dim)
+    sk, sv = dev(prob.src_k), dev(prob.src_v)
+    tk = torch.full(oshape, float("nan"), dtype=torch.bfloat16, device="cuda")
+    tv = torch.full(oshape, float("nan"), dtype=torch.bfloat16, device="cuda")
+    io, keep = kvx.make_io(spec.batch, spec.src_tokens, sk, sv, tk, tv, cap,
+                           None if ident else prob.tgt_tokens, rp, ci, wt)
+    nws = kvx.kvx_staged_workspace_bytes(tr.plan, io, spec.tgt.n_layers)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    stages = [("pool", kvx.KVX_STAGE_POOL), ("project", kvx.KVX_STAGE_PROJECT),
+              ("store", kvx.KVX_STAGE_STORE)]
+
+    def staged_step():
+        for _, m in stages:
+            kvx.kvx_translate_staged(tr.plan, io, ws, stages=m, stream=stream)
+
+    t0 = time.perf_counter()
+    calls = 0
+    while time.perf_counter() - t0 < args.settle_s:
+        staged_step()
+        kvx.kvx_translate(tr.plan, io, stream)
+        calls += 1
+        torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        staged_step()
+    torch.cuda.synchronize()
+    if any(torch.isnan(x[:, b, :, :int(t)]).any() for x in (tk, tv)
+           for b, t in enumerate(prob.tgt_tokens)):
+        print("bench.py: staged output has unwritten rows", file=sys.stderr)
+        sys.exit(1)
+    # events on the launch stream around every stage launch
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in stages] for _ in range(args.steps)]
+    evf = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        for j, (_, m) in enumerate(stages):
+            ev[i][j][0].record(stream)
+            kvx.kvx_translate_staged(tr.plan, io, ws, stages=m, stream=stream)
+            ev[i][j][1].record(stream)
+    for i in range(args.steps):
+        evf[i][0].record(stream)
+        kvx.kvx_translate(tr.plan, io, stream)
+        evf[i][1].record(stream)
+    torch.cuda.synchronize()
+    ms_stage = [sum(ev[i][j][0].elapsed_time(ev[i][j][1]) for i in range(args.steps)) / args.steps
+                for j in range(len(stages))]
+    ms_fused = sum(a.elapsed_time(b) for a, b in evf) / args.steps
+    by = staged_bytes(spec, prob, prec == kvx.KVX_PREC_BF16X2)
+    alg = algorithmic(spec, prob)
+    per = {}
+    for (name, _), ms in zip(stages, ms_stage):
+        gbs = by[name] / (ms * 1e-3) / 1e9
+        per[name] = {"ms": round(ms, 5), "bytes": by[name], "gbs": round(gbs, 1),
+                     "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+    tfs = by["flops_issued"] / (ms_stage[1] * 1e-3) / 1e12
+    per["project"]["mfma_tflops_issued"] = round(tfs, 1)
+    per["project"]["mfma_frac_issued"] = round(tfs / MFMA_BF16_PEAK_TFS, 4)
+    total = sum(ms_stage)
+    tokens = spec.batch * spec.src_tokens
+    out = {
+        "metric": "staged translation: per-stage ms and GB/s (pool, project, store) beside "
+                  "the fused kernel",
+        "value": round(tokens / (total * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(total, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": spec.name, "src_tokens": spec.src_tokens,
+                   "tgt_tokens": int(prob.tgt_tokens.sum()), "batch": spec.batch,
+                   "precision": args.precision, "parallelism": "single GPU"},
+        "stages": per,
+        "fused": {"ms": round(ms_fused, 5), "bytes": alg["bytes"],
+                  "gbs": round(alg["bytes"] / (ms_fused * 1e-3) / 1e9, 1)},
+        "staged_over_fused": round(total / ms_fused, 3),
+        "workspace_bytes": nws,
+    }
+    print(json.dumps(out), flush=True)
+    del keep
     tr.close()
 
 

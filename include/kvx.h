@@ -27,6 +27,7 @@
 #ifndef KVX_H
 #define KVX_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -242,6 +243,46 @@ typedef struct {
 } kvx_plan_info;
 
 kvx_status kvx_plan_query(const kvx_plan* plan, kvx_plan_info* info);
+
+/* Staged (unfused) translation: the operator of Section 4 as three launches
+ * that pass their intermediates through a caller-provided device workspace,
+ * for measuring each stage's memory throughput against the fused kernel and as
+ * an independent path to check it:
+ *   KVX_STAGE_POOL     source RoPE removal on K and pooling over each target
+ *                      row's alignment entries (fp32), written to the
+ *                      workspace as bf16 planes hi and, unless the plan's
+ *                      precision is KVX_PREC_BF16 or the operand is an
+ *                      identity-aligned V, lo = bf16(z - hi);
+ *   KVX_STAGE_PROJECT  U = Z W^T per (target layer, K|V), fp32, on the
+ *                      matrix cores;
+ *   KVX_STAGE_STORE    bias, target RoPE on K, bf16 rounding, store into
+ *                      the target cache (contiguous or paged).
+ * Same arguments, layouts and validation as kvx_translate, for plans on the
+ * fused kernel (bf16) with precision BF16X2, BF16 or BF16X2_OUTLIER (the
+ * latter computed as BF16X2); other plans return KVX_EUNSUPPORTED, as do
+ * buffers or strides that are not 16-byte aligned.
+ * Workspace: device memory, 16-byte aligned, owned by the caller, not read
+ * before it is written; kvx_staged_workspace_bytes gives the bytes that
+ * `layers` target layers take for this io (Z: 2 x 2 x rows x din bf16, U:
+ * 2 x rows x dout fp32 per layer, rows = the target rows of up to 64
+ * contexts, each rounded up to 128).  A smaller workspace runs the layers in
+ * groups (KVX_ESHAPE if one layer does not fit).  stages: a non-zero subset
+ * of KVX_STAGE_ALL; anything but KVX_STAGE_ALL requires a workspace for all
+ * target layers and batch <= 64 (KVX_EINVAL otherwise), and later stages
+ * must be called with the same io and workspace after the earlier ones
+ * (stream order).  Calls sharing a workspace must not overlap. */
+typedef enum {
+  KVX_STAGE_POOL = 1,
+  KVX_STAGE_PROJECT = 2,
+  KVX_STAGE_STORE = 4,
+  KVX_STAGE_ALL = 7
+} kvx_stage;
+
+kvx_status kvx_staged_workspace_bytes(const kvx_plan* plan, const kvx_io* io, int32_t layers,
+                                      size_t* bytes);
+
+kvx_status kvx_translate_staged(const kvx_plan* plan, const kvx_io* io, void* workspace,
+                                size_t workspace_bytes, uint32_t stages, void* stream);
 
 #ifdef __cplusplus
 }

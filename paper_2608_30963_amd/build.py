@@ -45,14 +45,15 @@ def _check(r, what):
 
 def build(out: str = LIB, verbose: bool = False) -> str:
     """Compile the host library, the translator fit, the translator-variant
-    composition and the fused kernel's
+    composition, the staged (unfused) translation and the fused kernel's
     three precision variants as separate objects (in parallel), then link
     libkvx.so."""
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     units = [("kvx", os.path.join(CSRC, "kvx.hip"), []),
              ("fit", os.path.join(CSRC, "fit.hip"), []),
-             ("compose", os.path.join(CSRC, "compose.hip"), [])]
+             ("compose", os.path.join(CSRC, "compose.hip"), []),
+             ("staged", os.path.join(CSRC, "staged.hip"), [])]
     for i, name in enumerate(("bf16x2", "bf16", "f16")):
         units.append((f"fused_{name}", os.path.join(CSRC, "fused_launch.hip"),
                       [f"-DKVX_LAUNCH_PREC={i}"]))

@@ -26,14 +26,14 @@ void launch_pspi(bool identity, bool ds128, int grid, hipStream_t st, const Fuse
 
 // tile order (contiguous ranges, interleaved, or resident) as a template
 // argument; the host picks the resident order only for span maps with
-// several N tiles (cached source loads)
+// several N tiles, and runs it with streaming source loads
 template <int PREC, bool STREAM, bool PAGED>
 void launch_psp(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
   if (a.interleave == 1) {
     launch_pspi<PREC, STREAM, PAGED, 1>(identity, ds128, grid, st, a);
     return;
   }
-  if constexpr (!STREAM) {
+  if constexpr (STREAM) {
     if (a.interleave == 2) {
       launch_pspi<PREC, STREAM, PAGED, 2>(identity, ds128, grid, st, a);
       return;
@@ -50,11 +50,12 @@ void launch_ps(bool identity, bool ds128, int grid, hipStream_t st, const FusedA
     launch_psp<PREC, STREAM, false>(identity, ds128, grid, st, a);
 }
 
-// Streaming source loads when a single N tile covers the output (no tile
-// re-reads a source row); cached loads otherwise.
+// Streaming source loads when no tile re-reads a source row: a single N tile
+// covers the output, or the resident order transforms a row tile once for
+// all its N tiles; cached loads otherwise.
 template <int PREC>
 void launch_p(bool identity, bool ds128, int grid, hipStream_t st, const FusedArgs& a) {
-  if (a.n_tiles == 1)
+  if (a.n_tiles == 1 || a.interleave == 2)
     launch_ps<PREC, true>(identity, ds128, grid, st, a);
   else
     launch_ps<PREC, false>(identity, ds128, grid, st, a);

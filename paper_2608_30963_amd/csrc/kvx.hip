@@ -14,6 +14,7 @@
 #include "kernel_mfma.h"
 #include "fused_launch.h"
 #include "kernel_tiled.h"
+#include "staged.h"
 
 using namespace kvx;
 
@@ -416,26 +417,36 @@ kvx_status validate_blocks(const kvx_io& io, const std::vector<int32_t>& ttok, h
   return KVX_OK;
 }
 
-}  // namespace
+// A call's arguments with the default strides filled in and the target rows
+// of every context; rows == 0: nothing to do.
+struct Call {
+  kvx_io io;
+  bool identity = false, paged = false;
+  std::vector<int32_t> ttok;
+  int64_t rows = 0;
+};
 
-extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void* stream) {
+kvx_status prepare_call(const kvx_plan* p, const kvx_io* io_in, Call& c) {
   if (!p || !io_in) return KVX_EINVAL;
-  kvx_io io = *io_in;
+  kvx_io& io = c.io;
+  io = *io_in;
   if (io.batch < 0 || io.src_tokens < 0 || io.tgt_capacity < 0) return KVX_EINVAL;
   if (io.batch == 0) return KVX_OK;
   const bool identity = io.tgt_tokens == nullptr;
   const bool paged = io.block_table != nullptr;
+  c.identity = identity;
+  c.paged = paged;
   if (paged && (io.block_size <= 0 || io.max_blocks <= 0 || io.num_blocks <= 0))
     return KVX_EINVAL;
   // rows a context may hold in the target layout
   const int64_t cap = paged ? int64_t(io.max_blocks) * io.block_size : io.tgt_capacity;
-  std::vector<int32_t> ttok(io.batch);
+  c.ttok.assign(io.batch, 0);
   int64_t rows = 0;
   for (int b = 0; b < io.batch; ++b) {
     const int32_t t = identity ? io.src_tokens : io.tgt_tokens[b];
     if (t < 0) return KVX_EINVAL;
     if (t > cap) return KVX_ESHAPE;
-    ttok[b] = t;
+    c.ttok[b] = t;
     rows += t;
   }
   if (rows == 0) return KVX_OK;
@@ -443,8 +454,8 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
   if (!identity && (!io.row_ptr || !io.col_idx || !io.weight)) return KVX_EINVAL;
   if (rows > INT32_MAX / 2) return KVX_ESHAPE;
 
-  const int64_t Ls = p->src.n_layers, Hs = p->src.n_kv_heads, Ds = p->src.head_dim;
-  const int64_t Lt = p->tgt.n_layers, Ht = p->tgt.n_kv_heads, Dt = p->tgt.head_dim;
+  const int64_t Hs = p->src.n_kv_heads, Ds = p->src.head_dim;
+  const int64_t Ht = p->tgt.n_kv_heads, Dt = p->tgt.head_dim;
   const int64_t B = io.batch;
   auto all_zero = [](const int64_t* s) { return !s[0] && !s[1] && !s[2] && !s[3]; };
   if (all_zero(io.src_stride)) {
@@ -467,29 +478,51 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
   const int64_t tgt_rows = paged ? io.block_size : io.tgt_capacity;  // rows per token stride run
   if ((io.src_stride[3] < Ds && io.src_tokens > 1) || (io.tgt_stride[3] < Dt && tgt_rows > 1))
     return KVX_ESHAPE;
-  (void)Ls;
+  c.rows = rows;
+  return KVX_OK;
+}
 
-  hipStream_t st = static_cast<hipStream_t>(stream);
+// KVX_VALIDATE=1: check the device-resident alignment map and block table.
+kvx_status validate_call(const Call& c, bool csr, bool blocks, hipStream_t st) {
   const char* vmode = std::getenv("KVX_VALIDATE");
-  if (!identity && vmode && vmode[0] == '1') {
-    kvx_status s = validate_csr(io, rows, st);
+  if (!(vmode && vmode[0] == '1')) return KVX_OK;
+  if (csr && !c.identity) {
+    kvx_status s = validate_csr(c.io, c.rows, st);
     if (s != KVX_OK) return s;
   }
-  if (paged && vmode && vmode[0] == '1') {
-    kvx_status s = validate_blocks(io, ttok, st);
+  if (blocks && c.paged) {
+    kvx_status s = validate_blocks(c.io, c.ttok, st);
     if (s != KVX_OK) return s;
   }
+  return KVX_OK;
+}
+
+// 16-byte vector access needs 16-byte aligned rows and buffers.
+bool rows_aligned16(const kvx_io& io, int esz) {
+  for (int i = 0; i < 4; ++i)
+    if ((io.src_stride[i] * esz) % 16 || (io.tgt_stride[i] * esz) % 16) return false;
+  return aligned16(io.src_k) && aligned16(io.src_v) && aligned16(io.tgt_k) && aligned16(io.tgt_v);
+}
+
+}  // namespace
+
+extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void* stream) {
+  Call call;
+  kvx_status cs = prepare_call(p, io_in, call);
+  if (cs != KVX_OK || call.rows == 0) return cs;
+  const kvx_io& io = call.io;
+  const bool identity = call.identity, paged = call.paged;
+  const std::vector<int32_t>& ttok = call.ttok;
+  const int64_t rows = call.rows;
+  const int64_t Hs = p->src.n_kv_heads, Ds = p->src.head_dim;
+  const int64_t Lt = p->tgt.n_layers, Ht = p->tgt.n_kv_heads, Dt = p->tgt.head_dim;
+  const int64_t B = io.batch;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  cs = validate_call(call, true, true, st);
+  if (cs != KVX_OK) return cs;
 
   const int esz = p->dtype == KVX_F32 ? 4 : 2;
-  bool fused = p->kernel == kFused;
-  if (fused) {
-    // 16-byte vector access needs 16-byte aligned rows
-    for (int i = 0; i < 4; ++i)
-      if ((io.src_stride[i] * esz) % 16 || (io.tgt_stride[i] * esz) % 16) fused = false;
-    if (!aligned16(io.src_k) || !aligned16(io.src_v) || !aligned16(io.tgt_k) ||
-        !aligned16(io.tgt_v))
-      fused = false;
-  }
+  bool fused = p->kernel == kFused && rows_aligned16(io, esz);
   // the fused kernel addresses a context's rows of one head with 32-bit byte
   // offsets (contiguous layout)
   if (fused && !paged && int64_t(io.tgt_capacity) * io.tgt_stride[3] * esz > INT32_MAX)
@@ -606,6 +639,142 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e);
+  }
+  return KVX_OK;
+}
+
+namespace {
+
+// Rows of the staged path's intermediates for one group of contexts: row
+// tiles of 128 per context; the largest over the call's groups.
+int64_t staged_rows(const Call& c) {
+  int64_t best = 0;
+  for (int64_t b0 = 0; b0 < c.io.batch; b0 += kMaxBatch) {
+    int64_t r = 0;
+    for (int64_t b = b0; b < c.io.batch && b < b0 + kMaxBatch; ++b)
+      r += (c.ttok[b] + kStageRows - 1) / kStageRows * kStageRows;
+    best = r > best ? r : best;
+  }
+  return best;
+}
+
+// Workspace bytes per target layer: Z (K and V, hi and lo planes, bf16) and
+// U (K and V, fp32).
+size_t staged_layer_bytes(const kvx_plan* p, int64_t rows) {
+  return size_t(2) * (size_t(2) * rows * p->din * sizeof(bf16_t) + size_t(rows) * p->dout * 4);
+}
+
+kvx_status staged_plan_ok(const kvx_plan* p) {
+  if (p->kernel != kFused || p->precision == KVX_PREC_F16) return KVX_EUNSUPPORTED;
+  return KVX_OK;
+}
+
+}  // namespace
+
+extern "C" kvx_status kvx_staged_workspace_bytes(const kvx_plan* p, const kvx_io* io_in,
+                                                 int32_t layers, size_t* bytes) {
+  if (bytes) *bytes = 0;
+  if (!p || !io_in || !bytes || layers < 1) return KVX_EINVAL;
+  kvx_status s = staged_plan_ok(p);
+  if (s != KVX_OK) return s;
+  Call call;
+  s = prepare_call(p, io_in, call);
+  if (s != KVX_OK || call.rows == 0) return s;
+  const int32_t lg = layers < p->tgt.n_layers ? layers : p->tgt.n_layers;
+  *bytes = staged_layer_bytes(p, staged_rows(call)) * lg;
+  return KVX_OK;
+}
+
+extern "C" kvx_status kvx_translate_staged(const kvx_plan* p, const kvx_io* io_in, void* workspace,
+                                           size_t workspace_bytes, uint32_t stages,
+                                           void* stream) {
+  if (!p || !io_in) return KVX_EINVAL;
+  if (stages == 0 || (stages & ~uint32_t(KVX_STAGE_ALL)) != 0) return KVX_EINVAL;
+  kvx_status s = staged_plan_ok(p);
+  if (s != KVX_OK) return s;
+  Call call;
+  s = prepare_call(p, io_in, call);
+  if (s != KVX_OK || call.rows == 0) return s;
+  const kvx_io& io = call.io;
+  if (!rows_aligned16(io, 2)) return KVX_EUNSUPPORTED;
+  if (!workspace || !aligned16(workspace)) return KVX_EINVAL;
+  const int64_t Lt = p->tgt.n_layers, B = io.batch;
+  const int64_t rows_max = staged_rows(call);
+  const size_t per_layer = staged_layer_bytes(p, rows_max);
+  int64_t lg = static_cast<int64_t>(workspace_bytes / per_layer);
+  if (lg < 1) return KVX_ESHAPE;
+  lg = lg < Lt ? lg : Lt;
+  // a subset of the stages reads or leaves intermediates in the workspace,
+  // so one pass must cover every layer and context
+  if (stages != KVX_STAGE_ALL && (lg < Lt || B > kMaxBatch)) return KVX_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  s = validate_call(call, (stages & KVX_STAGE_POOL) != 0, (stages & KVX_STAGE_STORE) != 0, st);
+  if (s != KVX_OK) return s;
+
+  StagedArgs a{};
+  a.ss = Strides{io.src_stride[0], io.src_stride[1], io.src_stride[2], io.src_stride[3]};
+  a.ts = Strides{io.tgt_stride[0], io.tgt_stride[1], io.tgt_stride[2], io.tgt_stride[3]};
+  a.wp[0] = static_cast<const bf16x8*>(p->w[0]);
+  a.wp[1] = static_cast<const bf16x8*>(p->w[1]);
+  a.bias[0] = p->bias[0];
+  a.bias[1] = p->bias[1];
+  a.layer_map = p->layer_map;
+  a.fs = p->fs;
+  a.ft = p->ft;
+  a.row_ptr = call.identity ? nullptr : io.row_ptr;
+  a.col_idx = io.col_idx;
+  a.weight = io.weight;
+  a.mix = p->mix;
+  a.hs = p->src.n_kv_heads;
+  a.ds = p->src.head_dim;
+  a.ht = p->tgt.n_kv_heads;
+  a.dt = p->tgt.head_dim;
+  a.din = p->din;
+  a.dout = p->dout;
+  // operands as the fused kernel's precision modes round them: two planes
+  // for computed operands unless the plan rounds them once (BF16); an
+  // identity-aligned V is exact
+  const bool split = p->precision != KVX_PREC_BF16;
+  a.planes[0] = split ? 2 : 1;
+  a.planes[1] = split && !call.identity ? 2 : 1;
+  int64_t row_base = 0;
+  for (int64_t b0 = 0; b0 < B; b0 += kMaxBatch) {
+    const int nb = static_cast<int>(B - b0 < kMaxBatch ? B - b0 : kMaxBatch);
+    BatchArgs ba{};
+    ba.n = nb;
+    int tiles = 0;
+    for (int i = 0; i < nb; ++i) {
+      ba.tile_start[i] = tiles;
+      ba.t_tgt[i] = call.ttok[b0 + i];
+      ba.row_base[i] = static_cast<int32_t>(row_base);
+      row_base += call.ttok[b0 + i];
+      tiles += (call.ttok[b0 + i] + kStageRows - 1) / kStageRows;
+    }
+    ba.tile_start[nb] = tiles;
+    if (tiles == 0) continue;
+    a.ba = ba;
+    a.tiles = tiles;
+    a.rows_p = tiles * kStageRows;
+    a.src[0] = static_cast<const bf16_t*>(io.src_k) + b0 * io.src_stride[1];
+    a.src[1] = static_cast<const bf16_t*>(io.src_v) + b0 * io.src_stride[1];
+    // paged: blocks are shared by all contexts; the table row moves instead
+    const int64_t toff = call.paged ? 0 : b0 * io.tgt_stride[1];
+    a.tgt[0] = static_cast<bf16_t*>(io.tgt_k) + toff;
+    a.tgt[1] = static_cast<bf16_t*>(io.tgt_v) + toff;
+    a.pg = Paging{call.paged ? io.block_table + b0 * io.max_blocks : nullptr,
+                  call.paged ? io.block_size : 1, call.paged ? io.max_blocks : 0};
+    for (int64_t l0 = 0; l0 < Lt; l0 += lg) {
+      a.l0 = static_cast<int32_t>(l0);
+      a.nl = static_cast<int32_t>(Lt - l0 < lg ? Lt - l0 : lg);
+      a.z = static_cast<bf16_t*>(workspace);
+      a.u = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                     size_t(a.nl) * 2 * 2 * a.rows_p * p->din * sizeof(bf16_t));
+      if (stages & KVX_STAGE_POOL) launch_stage_pool(a, st);
+      if (stages & KVX_STAGE_PROJECT) launch_stage_project(a, st);
+      if (stages & KVX_STAGE_STORE) launch_stage_store(a, st);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return hip_fail(e);
+    }
   }
   return KVX_OK;
 }

@@ -26,11 +26,13 @@ KVX_OK, KVX_EINVAL, KVX_ESHAPE, KVX_EUNSUPPORTED, KVX_ENOMEM, KVX_EHIP, KVX_EDAT
 KVX_F32, KVX_BF16 = 0, 1
 KVX_PREC_BF16X2, KVX_PREC_BF16, KVX_PREC_F16, KVX_PREC_BF16X2_OUTLIER = 0, 1, 2, 3
 KVX_FACTORS_LOWRANK, KVX_FACTORS_MIXTURE = 1, 2
+KVX_STAGE_POOL, KVX_STAGE_PROJECT, KVX_STAGE_STORE, KVX_STAGE_ALL = 1, 2, 4, 7
 
 # Exported C symbols, as declared in include/kvx.h and include/kvx_fit.h.
 SYMBOLS = ("kvx_plan_create", "kvx_plan_create_factored", "kvx_translate", "kvx_plan_destroy",
            "kvx_status_string",
-           "kvx_last_hip_error", "kvx_plan_query", "kvx_fit_create", "kvx_fit_accumulate",
+           "kvx_last_hip_error", "kvx_plan_query", "kvx_staged_workspace_bytes",
+           "kvx_translate_staged", "kvx_fit_create", "kvx_fit_accumulate",
            "kvx_fit_solve", "kvx_fit_solve_noalloc", "kvx_fit_reset", "kvx_fit_rows",
            "kvx_fit_query", "kvx_fit_destroy")
 
@@ -128,6 +130,12 @@ def load(path: str = LIB_PATH):
     lib.kvx_last_hip_error.restype = C.c_int32
     lib.kvx_plan_query.argtypes = [C.c_void_p, C.POINTER(PlanInfo)]
     lib.kvx_plan_query.restype = C.c_int
+    lib.kvx_staged_workspace_bytes.argtypes = [C.c_void_p, C.POINTER(IO), C.c_int32,
+                                               C.POINTER(C.c_size_t)]
+    lib.kvx_staged_workspace_bytes.restype = C.c_int
+    lib.kvx_translate_staged.argtypes = [C.c_void_p, C.POINTER(IO), C.c_void_p, C.c_size_t,
+                                         C.c_uint32, C.c_void_p]
+    lib.kvx_translate_staged.restype = C.c_int
     lib.kvx_fit_create.argtypes = [C.POINTER(FitDesc), C.POINTER(C.c_void_p)]
     lib.kvx_fit_create.restype = C.c_int
     lib.kvx_fit_accumulate.argtypes = [C.c_void_p, C.POINTER(FitIO), C.c_void_p]
@@ -297,6 +305,44 @@ def kvx_translate(plan: int, io: IO, stream=None) -> int:
 def kvx_translate_status(plan, io: IO, stream_handle: int = 0) -> int:
     """Raw status of kvx_translate (no exception)."""
     return int(load().kvx_translate(C.c_void_p(plan), C.byref(io), C.c_void_p(stream_handle)))
+
+
+def kvx_staged_workspace_bytes(plan: int, io: IO, layers: int) -> int:
+    """Device bytes the staged translation's workspace needs for `layers`
+    target layers of this call."""
+    n = C.c_size_t(0)
+    st = load().kvx_staged_workspace_bytes(C.c_void_p(plan), C.byref(io), int(layers),
+                                           C.byref(n))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_staged_workspace_bytes")
+    return int(n.value)
+
+
+def kvx_translate_staged_status(plan: int, io: IO, workspace: int, workspace_bytes: int,
+                                stages: int = KVX_STAGE_ALL, stream_handle: int = 0) -> int:
+    """Raw status of kvx_translate_staged (no exception); `workspace` is a
+    device address."""
+    return int(load().kvx_translate_staged(C.c_void_p(plan), C.byref(io), C.c_void_p(workspace),
+                                           int(workspace_bytes), int(stages),
+                                           C.c_void_p(stream_handle)))
+
+
+def kvx_translate_staged(plan: int, io: IO, workspace, workspace_bytes: Optional[int] = None,
+                         stages: int = KVX_STAGE_ALL, stream=None) -> int:
+    """Enqueue the staged (three-launch) translation; `workspace` is a device
+    tensor (its size is passed unless `workspace_bytes` is given) or a
+    device address."""
+    if hasattr(workspace, "data_ptr"):
+        nbytes = workspace.numel() * workspace.element_size()
+        ptr = workspace.data_ptr()
+    else:
+        nbytes, ptr = workspace_bytes, int(workspace)
+    if workspace_bytes is not None:
+        nbytes = workspace_bytes
+    st = kvx_translate_staged_status(plan, io, ptr, nbytes, stages, _stream_handle(stream))
+    if st != KVX_OK:
+        raise KvxError(st, "kvx_translate_staged")
+    return st
 
 
 def kvx_plan_destroy(plan: Optional[int]) -> None:

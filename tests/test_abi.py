@@ -107,6 +107,25 @@ def test_translate_rejects_null_and_destroy_is_null_safe():
     kvx.kvx_plan_destroy(None)
 
 
+def test_staged_entries_reject_bad_arguments():
+    """Checked before the plan or any device memory is touched."""
+    lib = kvx.load()
+    io, keep = kvx.make_io(1, 4, 0x10, 0x10, 0x10, 0x10, 4)
+    n = C.c_size_t(99)
+    assert lib.kvx_staged_workspace_bytes(None, C.byref(io), 1, C.byref(n)) == kvx.KVX_EINVAL
+    assert n.value == 0
+    assert lib.kvx_staged_workspace_bytes(C.c_void_p(1), C.byref(io), 0, C.byref(n)) == \
+        kvx.KVX_EINVAL
+    assert lib.kvx_staged_workspace_bytes(C.c_void_p(1), C.byref(io), 1, None) == kvx.KVX_EINVAL
+    assert lib.kvx_translate_staged(None, C.byref(io), None, 0, kvx.KVX_STAGE_ALL, None) == \
+        kvx.KVX_EINVAL
+    assert lib.kvx_translate_staged(C.c_void_p(1), None, None, 0, kvx.KVX_STAGE_ALL, None) == \
+        kvx.KVX_EINVAL
+    for bad in (0, 8, 0xF):
+        assert lib.kvx_translate_staged(C.c_void_p(1), C.byref(io), None, 0, bad, None) == \
+            kvx.KVX_EINVAL
+
+
 def test_query_rejects_null():
     info = kvx.PlanInfo()
     assert kvx.load().kvx_plan_query(None, C.byref(info)) == kvx.KVX_EINVAL
