@@ -20,8 +20,9 @@
  * cache equals the distance before the target rotation.
  *
  * Work split: kvx_fit_accumulate forms Z and Y on the device and adds
- * Zt^T [Zt Y] into fp32 accumulators held by the fit (matrix cores, operands
- * split into two bf16 terms: relative product error about 2^-16);
+ * Zt^T [Zt Y] into fp32 accumulators held by the fit (matrix cores; operands
+ * that are not exact bf16 values are split into two bf16 terms: relative
+ * product error about 2^-16);
  * kvx_fit_solve factors each system in fp64 (Cholesky) and writes W and b.
  * Calls are stream-ordered; everything runs in HIP kernels.
  */
@@ -70,7 +71,8 @@ typedef struct kvx_fit kvx_fit;
 
 /* Allocate the fp32 accumulators (zeroed) and copy the layer map and RoPE
  * tables (synchronous, current HIP device).  Errors: KVX_EINVAL, KVX_ESHAPE,
- * KVX_EUNSUPPORTED (odd head_dim), KVX_ENOMEM, KVX_EHIP; *out = NULL then. */
+ * KVX_EUNSUPPORTED (a head_dim that is not a multiple of 16), KVX_ENOMEM,
+ * KVX_EHIP; *out = NULL then. */
 kvx_status kvx_fit_create(const kvx_fit_desc* desc, kvx_fit** out);
 
 /* Add one batch of paired caches to the accumulators (asynchronous on

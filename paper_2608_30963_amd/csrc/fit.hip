@@ -3,12 +3,15 @@
 // squared Frobenius distance).
 //
 // Device pipeline per batch of paired caches and group of target layers:
-//   fit_prepare  Z (pooled, source-de-rotated rows, plus a ones column for the
-//                bias) and Y (target rows de-rotated by the target RoPE) as
-//                feature-major bf16 planes hi/lo, X^T[plane][feature][row];
+//   fit_prepare  Z (pooled, source-de-rotated rows) and Y (target rows
+//                de-rotated by the target RoPE) as feature-major bf16 planes
+//                hi (and lo, unless the values are exact bf16),
+//                X^T[plane][feature][row]; adds the column sums of Z and Y
+//                and the row count (the bias column's entries) to the
+//                accumulators;
 //   fit_gram     acc[i][j] += sum_r X[r][i] X[r][j] for i over the Z features
 //                and j >= i over Z and Y (upper Z^T Z blocks and Z^T Y),
-//                v_mfma_f32_32x32x16_bf16 with hi*hi + hi*lo + lo*hi;
+//                v_mfma_f32_32x32x16_bf16 with hi*hi (+ hi*lo + lo*hi);
 // and once per solve:
 //   fit_solve    per system: A = Z^T Z + lam D (fp64), blocked Cholesky,
 //                forward and backward substitution for the Z^T Y columns,
@@ -33,6 +36,7 @@ namespace {
 
 constexpr int kFB = 128;       // Gram block edge (features)
 constexpr int kSlab = 32;      // rows per LDS slab of the Gram kernel
+constexpr int kPrepRows = 64;  // rows per workgroup of fit_prepare (rows padded to it)
 constexpr int kPitch = kSlab + 8;  // LDS pitch (bf16) of one feature's slab row
 constexpr int kFitBatch = 64;  // contexts per launch
 constexpr int kNB = 32;        // Cholesky panel width
@@ -66,9 +70,15 @@ struct PrepArgs {
   const double* fs;  // source theta / 2pi (zeros without RoPE)
   const double* ft;  // target theta / 2pi
   int32_t mix, hs, ds, ht, dt;
-  int32_t din, dout, din_p, dout_p, F, rp, nrows, l0, fit_bias;
-  int32_t src_rope, tgt_rope;
-  bf16_t* xt;  // [sys][2][F][rp], sys = (l - l0) * 2 + kv
+  int32_t din, dout, din_z, dout_p, F2, rp, nrows, l0;
+  int32_t tz, ty;          // job tiles of Z pairs and of Y pairs (then padding tiles)
+  int32_t pz[2], py[2];    // planes written per K|V: 2 (hi, lo) or 1 (exact bf16)
+  int32_t src_rope, tgt_rope, vec;
+  bf16_t* xt;  // [sys][2][F2][rp], sys = (l - l0) * 2 + kv
+  // bias sums (fit_bias): Z column sums into acc[sys][f][din], Y column sums
+  // into acc[sys][din][din_p + c], the row count into acc[sys][din][din]
+  float* acc;
+  int32_t din_p, F, sys0, fit_bias;
   FitCtx ctx;
 };
 
@@ -82,147 +92,216 @@ __device__ __forceinline__ int ctx_of(const FitCtx& c, int r) {
   return lo;
 }
 
-__device__ __forceinline__ void split_store(bf16_t* hi, bf16_t* lo, const float (&v)[8]) {
-  uint32_t h[4], l[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const bf16_t h0 = f32_to_bf16(v[2 * i]), h1 = f32_to_bf16(v[2 * i + 1]);
-    const bf16_t l0 = f32_to_bf16(v[2 * i] - bf16_to_f32(h0));
-    const bf16_t l1 = f32_to_bf16(v[2 * i + 1] - bf16_to_f32(h1));
-    h[i] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
-    l[i] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
-  }
-  *reinterpret_cast<uint4*>(hi) = make_uint4(h[0], h[1], h[2], h[3]);
-  *reinterpret_cast<uint4*>(lo) = make_uint4(l[0], l[1], l[2], l[3]);
-}
-
-// One thread: one job (a RoPE pair of Z, a pair of Y, or one padding / ones
-// feature) over 8 consecutive rows.  grid: x = job blocks, y = row groups of
-// 8 (grid-stride), z = systems of the layer group.
+// Eight consecutive elements as fp32: one 16-byte load (bf16) or two (fp32)
+// when `vec`, else element by element.
 template <typename T>
-__device__ __forceinline__ void prepare_rows(const PrepArgs& a, int job, int r0, int sys);
-
-template <typename T>
-__global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
-  const int job = blockIdx.x * 256 + threadIdx.x;
-  const int nz = a.din / 2, ny = a.dout / 2;
-  const int npad = (a.din_p - a.din) + (a.dout_p - a.dout);
-  if (job >= nz + ny + npad) return;
-  for (int r0 = blockIdx.y * 8; r0 < a.rp; r0 += gridDim.y * 8)
-    prepare_rows<T>(a, job, r0, blockIdx.z);
-}
-
-template <typename T>
-__device__ __forceinline__ void prepare_rows(const PrepArgs& a, int job, int r0, int sys) {
-  const int nz = a.din / 2, ny = a.dout / 2;
-  const int l = a.l0 + sys / 2;
-  const int kv = sys % 2;
-  bf16_t* base = a.xt + static_cast<int64_t>(sys) * 2 * a.F * a.rp;
-  bf16_t* lo_base = base + static_cast<int64_t>(a.F) * a.rp;
-  float v1[8], v2[8];
-  int f1, f2 = -1;
-  if (job < nz) {
-    // Z pair: mixed layer j, source head h, frequency i
-    const int half = a.ds / 2;
-    const int jh = job / half, i = job % half;
-    const int j = jh / a.hs, h = jh % a.hs;
-    const int ls = a.layer_map[l * a.mix + j];
-    f1 = jh * a.ds + i;
-    f2 = f1 + half;
-    const T* src = static_cast<const T*>(a.src[kv]) + ls * a.ss.l + h * a.ss.h + i;
-    const bool rot = kv == 0 && a.src_rope;
-    const double fr = a.fs[i];
+__device__ __forceinline__ void load8(const T* p, bool vec, float (&x)[8]);
+template <>
+__device__ __forceinline__ void load8<bf16_t>(const bf16_t* p, bool vec, float (&x)[8]) {
+  if (vec) {
+    const uint4 r = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int r = r0 + q;
-      float z1 = 0.f, z2 = 0.f;
-      if (r < a.nrows) {
-        const int b = ctx_of(a.ctx, r);
-        const int t = r - a.ctx.row0[b];
-        const T* sb = src + b * a.ss.b;
-        int e0 = 0, e1 = 1;
-        if (a.row_ptr) {
-          e0 = a.row_ptr[a.ctx.csr0[b] + t];
-          e1 = a.row_ptr[a.ctx.csr0[b] + t + 1];
-        }
-        for (int e = e0; e < e1; ++e) {
-          const int k = a.row_ptr ? a.col_idx[e] : t;
-          const float w = a.row_ptr ? a.weight[e] : 1.f;
-          const float x1 = load_f32<T>(sb + k * a.ss.t);
-          const float x2 = load_f32<T>(sb + k * a.ss.t + half);
-          float y1 = x1, y2 = x2;
-          if (rot) {
-            float c, s;
-            rope_cs(fr, k, c, s);
-            y1 = x1 * c + x2 * s;
-            y2 = x2 * c - x1 * s;
-          }
-          z1 += w * y1;
-          z2 += w * y2;
-        }
-      }
-      v1[q] = z1;
-      v2[q] = z2;
-    }
-  } else if (job < nz + ny) {
-    // Y pair: target head h, frequency i
-    const int p = job - nz;
-    const int half = a.dt / 2;
-    const int h = p / half, i = p % half;
-    f1 = a.din_p + h * a.dt + i;
-    f2 = f1 + half;
-    const T* tg = static_cast<const T*>(a.tgt[kv]) + l * a.ts.l + h * a.ts.h + i;
-    const bool rot = kv == 0 && a.tgt_rope;
-    const double fr = a.ft[i];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int r = r0 + q;
-      float y1 = 0.f, y2 = 0.f;
-      if (r < a.nrows) {
-        const int b = ctx_of(a.ctx, r);
-        const int t = r - a.ctx.row0[b];
-        const T* rowp = tg + b * a.ts.b + t * a.ts.t;
-        const float x1 = load_f32<T>(rowp), x2 = load_f32<T>(rowp + half);
-        y1 = x1;
-        y2 = x2;
-        if (rot) {
-          float c, s;
-          rope_cs(fr, t, c, s);
-          y1 = x1 * c + x2 * s;
-          y2 = x2 * c - x1 * s;
-        }
-      }
-      v1[q] = y1;
-      v2[q] = y2;
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
     }
   } else {
-    // padding features; the first one after Z is the ones column of the bias
-    const int p = job - nz - ny;
-    const int zpad = a.din_p - a.din;
-    f1 = p < zpad ? a.din + p : a.din_p + a.dout + (p - zpad);
-    const bool ones = a.fit_bias && f1 == a.din;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v1[q] = (ones && r0 + q < a.nrows) ? 1.f : 0.f;
+    for (int i = 0; i < 8; ++i) x[i] = bf16_to_f32(p[i]);
   }
-  split_store(base + static_cast<int64_t>(f1) * a.rp + r0,
-              lo_base + static_cast<int64_t>(f1) * a.rp + r0, v1);
-  if (f2 >= 0)
-    split_store(base + static_cast<int64_t>(f2) * a.rp + r0,
-                lo_base + static_cast<int64_t>(f2) * a.rp + r0, v2);
+}
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, bool vec, float (&x)[8]) {
+  if (vec) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = p[i];
+  }
+}
+
+// Feature (row of X^T) of local feature q of job tile jt, or -1: Z tiles hold
+// 64 RoPE pairs of the flattened (mixed layer, source head, frequency) list
+// (first members q < 64, second members 64 + q), Y tiles 64 pairs of the
+// (target head, frequency) list after the din_z Z features, padding tiles
+// 128 zero features (Z padding din .. din_z - 1, then Y padding).
+__device__ __forceinline__ int tile_feature(const PrepArgs& a, int jt, int q) {
+  const int m = q % 64, second = q / 64;
+  if (jt < a.tz) {
+    const int p = 64 * jt + m;
+    if (p >= a.din / 2) return -1;
+    const int half = a.ds / 2;
+    return (p / half) * a.ds + p % half + second * half;
+  }
+  if (jt < a.tz + a.ty) {
+    const int p = 64 * (jt - a.tz) + m;
+    if (p >= a.dout / 2) return -1;
+    const int half = a.dt / 2;
+    return a.din_z + (p / half) * a.dt + p % half + second * half;
+  }
+  int idx = 128 * (jt - a.tz - a.ty) + q;
+  if (idx < a.din_z - a.din) return a.din + idx;
+  idx -= a.din_z - a.din;
+  if (idx < a.dout_p - a.dout) return a.din_z + a.dout + idx;
+  return -1;
+}
+
+// One workgroup: one job tile (128 features) x 64 rows of one system.  The
+// rows are formed token-major (16-byte loads of 8 pairs, 8 lanes per 128-byte
+// row segment), transposed through LDS, and written feature-major, 8 lanes per
+// 128-byte run of one feature; each feature's sum over the tile's rows goes to
+// the bias accumulators.  grid: (job tiles, rp / 64, systems of the group).
+template <typename T>
+__global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
+  __shared__ float tr[128][65];  // [local feature][row]
+  const int jt = blockIdx.x, r0 = blockIdx.y * 64, sys = blockIdx.z;
+  const int l = a.l0 + sys / 2, kv = sys % 2;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const bool vec = a.vec != 0;
+  if (jt < a.tz + a.ty) {
+    const bool isz = jt < a.tz;
+    const int g = lane % 8;
+    const int npairs = isz ? a.din / 2 : a.dout / 2;
+    const int p0 = 64 * (isz ? jt : jt - a.tz) + 8 * g;  // 8 pairs of one head
+#pragma unroll 1
+    for (int u = 0; u < 2; ++u) {
+      const int i = lane / 8 + 8 * w + 32 * u;
+      const int r = r0 + i;
+      float v1[8], v2[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v1[q] = v2[q] = 0.f;
+      if (r < a.nrows && p0 < npairs) {
+        const int b = ctx_of(a.ctx, r);
+        const int t = r - a.ctx.row0[b];
+        if (isz) {
+          const int half = a.ds / 2;
+          const int jh = p0 / half, i0 = p0 % half;
+          const int j = jh / a.hs, h = jh % a.hs;
+          const int ls = a.layer_map[l * a.mix + j];
+          const T* sb = static_cast<const T*>(a.src[kv]) + ls * a.ss.l + b * a.ss.b +
+                        h * a.ss.h + i0;
+          const bool rot = kv == 0 && a.src_rope;
+          int e0 = 0, e1 = 1;
+          if (a.row_ptr) {
+            e0 = a.row_ptr[a.ctx.csr0[b] + t];
+            e1 = a.row_ptr[a.ctx.csr0[b] + t + 1];
+          }
+          for (int e = e0; e < e1; ++e) {
+            const int k = a.row_ptr ? a.col_idx[e] : t;
+            const float wt = a.row_ptr ? a.weight[e] : 1.f;
+            float x1[8], x2[8];
+            load8<T>(sb + k * a.ss.t, vec, x1);
+            load8<T>(sb + k * a.ss.t + half, vec, x2);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              float y1 = x1[q], y2 = x2[q];
+              if (rot) {
+                float c, sn;
+                rope_cs(a.fs[i0 + q], k, c, sn);
+                y1 = x1[q] * c + x2[q] * sn;
+                y2 = x2[q] * c - x1[q] * sn;
+              }
+              v1[q] += wt * y1;
+              v2[q] += wt * y2;
+            }
+          }
+        } else {
+          const int half = a.dt / 2;
+          const int h = p0 / half, i0 = p0 % half;
+          const T* rowp = static_cast<const T*>(a.tgt[kv]) + l * a.ts.l + b * a.ts.b +
+                          h * a.ts.h + t * a.ts.t + i0;
+          load8<T>(rowp, vec, v1);
+          load8<T>(rowp + half, vec, v2);
+          if (kv == 0 && a.tgt_rope) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              float c, sn;
+              rope_cs(a.ft[i0 + q], t, c, sn);
+              const float y1 = v1[q] * c + v2[q] * sn;
+              const float y2 = v2[q] * c - v1[q] * sn;
+              v1[q] = y1;
+              v2[q] = y2;
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        tr[8 * g + q][i] = v1[q];
+        tr[64 + 8 * g + q][i] = v2[q];
+      }
+    }
+  } else {
+    for (int idx = tid; idx < 128 * 64; idx += 256) tr[idx / 64][idx % 64] = 0.f;
+  }
+  __syncthreads();
+  // feature-major output: piece = (local feature, 8-row octet)
+  const int64_t plane = static_cast<int64_t>(a.F2) * a.rp;
+  bf16_t* base = a.xt + static_cast<int64_t>(sys) * 2 * plane;
+  float* acc = a.acc + static_cast<int64_t>(a.sys0 + sys) * a.din_p * a.F;
+#pragma unroll 1
+  for (int k = 0; k < 4; ++k) {
+    const int piece = tid + 256 * k;
+    const int q = piece / 8, oct = piece % 8;
+    const int f = tile_feature(a, jt, q);
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = tr[q][8 * oct + e];
+    // sum over the tile's 64 rows: the 8 lanes of one feature are adjacent
+    float sum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sum += v[e];
+    sum += __shfl_xor(sum, 1);
+    sum += __shfl_xor(sum, 2);
+    sum += __shfl_xor(sum, 4);
+    if (f < 0) continue;
+    const bool zf = f < a.din_z;
+    const bool two = (zf ? a.pz[kv] : a.py[kv]) == 2;
+    uint32_t h[4], lo[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bf16_t h0 = f32_to_bf16(v[2 * i]), h1 = f32_to_bf16(v[2 * i + 1]);
+      const bf16_t l0 = f32_to_bf16(v[2 * i] - bf16_to_f32(h0));
+      const bf16_t l1 = f32_to_bf16(v[2 * i + 1] - bf16_to_f32(h1));
+      h[i] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+      lo[i] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
+    }
+    bf16_t* dst = base + static_cast<int64_t>(f) * a.rp + r0 + 8 * oct;
+    *reinterpret_cast<uint4*>(dst) = make_uint4(h[0], h[1], h[2], h[3]);
+    if (two) *reinterpret_cast<uint4*>(dst + plane) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+    if (a.fit_bias && oct == 0 && jt < a.tz + a.ty) {
+      if (zf)
+        atomicAdd(acc + static_cast<int64_t>(f) * a.F + a.din, sum);
+      else
+        atomicAdd(acc + static_cast<int64_t>(a.din) * a.F + a.din_p + (f - a.din_z), sum);
+    }
+  }
+  if (a.fit_bias && jt == 0 && blockIdx.y == 0 && tid == 0)
+    atomicAdd(acc + static_cast<int64_t>(a.din) * a.F + a.din, static_cast<float>(a.nrows));
 }
 
 struct GramArgs {
-  const bf16_t* xt;   // [sys][2][F][rp]
+  const bf16_t* xt;   // [sys][2][F2][rp]
   float* acc;         // [sys_total][din_p][F]; this group starts at sys0
-  int32_t F, rp, nbi, nbj, sys0, nblk;
+  int32_t F2, rp, nbi, nbj, sys0, nblk;
+  int32_t din_z, din_p, F;
+  int32_t pz[2], py[2];  // operand planes per K|V (1: exact bf16, lo plane absent)
 };
 
-// One workgroup: one 128 x 128 block (bi, bj >= bi) of one system, all rows.
-// Work items are system-major and each XCD takes a contiguous range, so the
-// workgroups that re-read one system's operands share that XCD's L2.
-// Four waves in 2 x 2, each 64 x 64 (2 x 2 MFMA tiles).  Slabs of 32 rows of
-// both feature blocks (hi and lo planes) are staged through LDS, double
-// buffered; the next slab is loaded into registers during the MFMAs.
+// One workgroup: one 128 x 128 block (bi, bj >= bi) of one system, all rows:
+// bi over the Z features, bj over Z and Y (the bias column's sums come from
+// fit_prepare).  Work items are system-major and each XCD takes a contiguous
+// range, so the workgroups that re-read one system's operands share that
+// XCD's L2.  Four waves in 2 x 2, each 64 x 64 (2 x 2 MFMA tiles).  Slabs of
+// 32 rows of both feature blocks (hi and, for operands that have one, lo
+// planes) are staged through LDS, double buffered; the next slab is loaded
+// into registers during the MFMAs.  Products: hi*hi, plus hi*lo and lo*hi
+// when the B and the A operand have a lo plane (exact bf16 operands --
+// identity-aligned V, native V -- have none).
 __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sl[2][2][2][kFB * kPitch];  // [stage][A|B][plane]
   const int wid = xcd_remap(blockIdx.x, gridDim.x);
@@ -238,8 +317,11 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
   const int lane = tid & 63;
   const int w = tid >> 6;
   const int wi = w / 2, wj = w % 2;
-  const bf16_t* xs = a.xt + static_cast<int64_t>(sys) * 2 * a.F * a.rp;
-  const int64_t plane = static_cast<int64_t>(a.F) * a.rp;
+  const bf16_t* xs = a.xt + static_cast<int64_t>(sys) * 2 * a.F2 * a.rp;
+  const int64_t plane = static_cast<int64_t>(a.F2) * a.rp;
+  const int kv = (a.sys0 + sys) % 2;
+  const bool lo_a = a.pz[kv] == 2;
+  const bool lo_b = (bj * kFB < a.din_z ? a.pz[kv] : a.py[kv]) == 2;
 
   // loader: piece p = tid + 256 * u (u < 2) of a 128-feature x 32-row slab
   // plane: feature p / 4, 16-byte column p % 4; 2 blocks x 2 planes x 2.
@@ -252,25 +334,27 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
     for (int ab = 0; ab < 2; ++ab)
 #pragma unroll
       for (int pl = 0; pl < 2; ++pl)
+        if (pl == 0 || (ab ? lo_b : lo_a))
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int p = tid + 256 * u;
-          const int f = (ab ? bj : bi) * kFB + p / 4;
-          ld[set][ab][pl][u] = *reinterpret_cast<const u32x4*>(
-              xs + pl * plane + static_cast<int64_t>(f) * a.rp + r0 + (p % 4) * 8);
-        }
+          for (int u = 0; u < 2; ++u) {
+            const int p = tid + 256 * u;
+            const int f = (ab ? bj : bi) * kFB + p / 4;
+            ld[set][ab][pl][u] = *reinterpret_cast<const u32x4*>(
+                xs + pl * plane + static_cast<int64_t>(f) * a.rp + r0 + (p % 4) * 8);
+          }
   };
   auto store_slab = [&](int set, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int ab = 0; ab < 2; ++ab)
 #pragma unroll
       for (int pl = 0; pl < 2; ++pl)
+        if (pl == 0 || (ab ? lo_b : lo_a))
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int p = tid + 256 * u;
-          *reinterpret_cast<u32x4*>(&sl[st][ab][pl][(p / 4) * kPitch + (p % 4) * 8]) =
-              ld[set][ab][pl][u];
-        }
+          for (int u = 0; u < 2; ++u) {
+            const int p = tid + 256 * u;
+            *reinterpret_cast<u32x4*>(&sl[st][ab][pl][(p / 4) * kPitch + (p % 4) * 8]) =
+                ld[set][ab][pl][u];
+          }
   };
 
   f32x16 acc[2][2];
@@ -297,20 +381,24 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int pl = 0; pl < 2; ++pl) {
-          fa[t][pl] = *reinterpret_cast<const bf16x8*>(
-              &sl[st][0][pl][(wi * 64 + t * 32 + lane % 32) * kPitch + ks * 16 + 8 * (lane / 32)]);
-          fb[t][pl] = *reinterpret_cast<const bf16x8*>(
-              &sl[st][1][pl][(wj * 64 + t * 32 + lane % 32) * kPitch + ks * 16 + 8 * (lane / 32)]);
+          if (pl == 0 || lo_a)
+            fa[t][pl] = *reinterpret_cast<const bf16x8*>(
+                &sl[st][0][pl][(wi * 64 + t * 32 + lane % 32) * kPitch + ks * 16 + 8 * (lane / 32)]);
+          if (pl == 0 || lo_b)
+            fb[t][pl] = *reinterpret_cast<const bf16x8*>(
+                &sl[st][1][pl][(wj * 64 + t * 32 + lane % 32) * kPitch + ks * 16 + 8 * (lane / 32)]);
         }
-      // hi*hi, hi*lo, lo*hi; consecutive MFMAs use different accumulators
+      // hi*hi, hi*lo, lo*hi (the last two for operands with a lo plane);
+      // consecutive MFMAs use different accumulators
 #pragma unroll
       for (int term = 0; term < 3; ++term)
+        if (term == 0 || (term == 1 ? lo_b : lo_a))
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+          for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                fa[i][term == 2 ? 1 : 0], fb[j][term == 1 ? 1 : 0], acc[i][j], 0, 0, 0);
+            for (int j = 0; j < 2; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  fa[i][term == 2 ? 1 : 0], fb[j][term == 1 ? 1 : 0], acc[i][j], 0, 0, 0);
     }
     if (s + 1 < nslab) store_slab(set ^ 1, st ^ 1);
     __syncthreads();
@@ -322,7 +410,7 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
   }
   if (s < nslab) body(s, 0);
   // D register v of lane l: row 8*(v/4) + 4*(l/32) + v%4, column l%32
-  float* out = a.acc + static_cast<int64_t>(a.sys0 + sys) * (a.nbi * kFB) * a.F;
+  float* out = a.acc + static_cast<int64_t>(a.sys0 + sys) * a.din_p * a.F;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -330,7 +418,8 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = bi * kFB + wi * 64 + i * 32 + 8 * (v / 4) + 4 * (lane / 32) + v % 4;
-        const int col = bj * kFB + wj * 64 + j * 32 + lane % 32;
+        const int f = bj * kFB + wj * 64 + j * 32 + lane % 32;  // feature of X^T
+        const int col = f < a.din_z ? f : a.din_p + (f - a.din_z);
         float* q = out + static_cast<int64_t>(row) * a.F + col;
         *q += acc[i][j][v];
       }
@@ -602,6 +691,7 @@ struct kvx_fit {
   kvx_model src{}, tgt{};
   int32_t mix = 1, dtype = KVX_BF16, fit_bias = 1;
   int32_t din = 0, dout = 0, din_p = 0, dout_p = 0, F = 0, n = 0;
+  int32_t din_z = 0, F2 = 0;  // prepared operands: Z features (padded), Z + Y
   int32_t src_rope = 0, tgt_rope = 0;
   int32_t* layer_map = nullptr;
   double* fs = nullptr;
@@ -623,7 +713,8 @@ kvx_status kvx_fit_create(const kvx_fit_desc* d, kvx_fit** out) {
   if (!valid_side(d->src) || !valid_side(d->tgt) || d->mix < 1) return KVX_EINVAL;
   if (d->dtype != KVX_F32 && d->dtype != KVX_BF16) return KVX_EINVAL;
   if (d->fit_bias != 0 && d->fit_bias != 1) return KVX_EINVAL;
-  if (d->src.head_dim % 2 || d->tgt.head_dim % 2) return KVX_EUNSUPPORTED;
+  // 8 RoPE pairs per 16-byte piece of a head
+  if (d->src.head_dim % 16 || d->tgt.head_dim % 16) return KVX_EUNSUPPORTED;
   const int64_t lt = d->tgt.n_layers;
   for (int64_t i = 0; i < lt * d->mix; ++i)
     if (d->layer_map[i] < 0 || d->layer_map[i] >= d->src.n_layers) return KVX_EINVAL;
@@ -653,6 +744,8 @@ kvx_status kvx_fit_create(const kvx_fit_desc* d, kvx_fit** out) {
   f->din_p = static_cast<int32_t>(round_up(f->n, kFB));
   f->dout_p = static_cast<int32_t>(round_up(dout, kFB));
   f->F = f->din_p + f->dout_p;
+  f->din_z = static_cast<int32_t>(round_up(f->din, kFB));
+  f->F2 = f->din_z + f->dout_p;
   f->src_rope = (d->src.inv_freq || d->src.rope_base > 0) ? 1 : 0;
   f->tgt_rope = (d->tgt.inv_freq || d->tgt.rope_base > 0) ? 1 : 0;
   hipError_t e = hipGetDevice(&f->device);
@@ -724,6 +817,20 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
     return KVX_ESHAPE;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int esz = f->dtype == KVX_F32 ? 4 : 2;
+  // 16-byte loads of 8 pairs need 8-element aligned rows and buffers
+  bool vec = (reinterpret_cast<uintptr_t>(io.src_k) | reinterpret_cast<uintptr_t>(io.src_v) |
+              reinterpret_cast<uintptr_t>(io.tgt_k) | reinterpret_cast<uintptr_t>(io.tgt_v)) %
+                 16 == 0;
+  for (int i = 0; i < 4; ++i)
+    if (io.src_stride[i] % 8 || io.tgt_stride[i] % 8) vec = false;
+  // operand planes: bf16 values that are exact (identity-aligned, unrotated
+  // source rows; unrotated native rows) need no lo plane
+  int planes_z[2], planes_y[2];
+  for (int kv = 0; kv < 2; ++kv) {
+    const bool bf = f->dtype == KVX_BF16;
+    planes_z[kv] = bf && identity && (kv == 1 || !f->src_rope) ? 1 : 2;
+    planes_y[kv] = bf && (kv == 1 || !f->tgt_rope) ? 1 : 2;
+  }
   const char* tenv = std::getenv("KVX_FIT_TIMING");
   const bool timing = tenv && tenv[0] == '1';
 
@@ -741,9 +848,9 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
     }
     ctx.row0[nb] = r;
     if (r == 0) continue;
-    const int32_t rp = static_cast<int32_t>(round_up(r, kSlab));
+    const int32_t rp = static_cast<int32_t>(round_up(r, kPrepRows));
     // layer groups sized so the prepared operands fit in 1 GiB
-    const size_t per_layer = size_t(2) * 2 * f->F * rp * sizeof(bf16_t);
+    const size_t per_layer = size_t(2) * 2 * f->F2 * rp * sizeof(bf16_t);
     const int64_t lg = std::max<int64_t>(1, std::min<int64_t>(Lt, (size_t(1) << 30) / per_layer));
     const size_t need = per_layer * lg;
     if (need > f->prep_bytes) {
@@ -780,19 +887,30 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
       pa.dt = static_cast<int32_t>(Dt);
       pa.din = f->din;
       pa.dout = f->dout;
-      pa.din_p = f->din_p;
+      pa.din_z = f->din_z;
       pa.dout_p = f->dout_p;
-      pa.F = f->F;
+      pa.F2 = f->F2;
       pa.rp = rp;
       pa.nrows = r;
       pa.l0 = static_cast<int32_t>(l0);
-      pa.fit_bias = f->fit_bias;
+      pa.tz = (f->din / 2 + 63) / 64;
+      pa.ty = (f->dout / 2 + 63) / 64;
+      for (int kv = 0; kv < 2; ++kv) {
+        pa.pz[kv] = planes_z[kv];
+        pa.py[kv] = planes_y[kv];
+      }
       pa.src_rope = f->src_rope;
       pa.tgt_rope = f->tgt_rope;
+      pa.vec = vec ? 1 : 0;
       pa.xt = static_cast<bf16_t*>(f->prep);
+      pa.acc = f->acc;
+      pa.din_p = f->din_p;
+      pa.F = f->F;
+      pa.sys0 = static_cast<int32_t>(l0 * 2);
+      pa.fit_bias = f->fit_bias;
       pa.ctx = ctx;
-      const int jobs = f->din / 2 + f->dout / 2 + (f->din_p - f->din) + (f->dout_p - f->dout);
-      const dim3 pg((jobs + 255) / 256, std::min(rp / 8, 32768), nl * 2);
+      const int npad = (f->din_z - f->din) + (f->dout_p - f->dout);
+      const dim3 pg(pa.tz + pa.ty + (npad + 127) / 128, rp / kPrepRows, nl * 2);
       if (f->dtype == KVX_F32)
         fit_prepare<float><<<pg, dim3(256), 0, st>>>(pa);
       else
@@ -801,10 +919,17 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
       GramArgs ga{};
       ga.xt = static_cast<const bf16_t*>(f->prep);
       ga.acc = f->acc;
-      ga.F = f->F;
+      ga.F2 = f->F2;
       ga.rp = rp;
-      ga.nbi = f->din_p / kFB;
-      ga.nbj = f->F / kFB;
+      ga.nbi = f->din_z / kFB;
+      ga.nbj = f->F2 / kFB;
+      ga.din_z = f->din_z;
+      ga.din_p = f->din_p;
+      ga.F = f->F;
+      for (int kv = 0; kv < 2; ++kv) {
+        ga.pz[kv] = planes_z[kv];
+        ga.py[kv] = planes_y[kv];
+      }
       ga.sys0 = static_cast<int32_t>(l0 * 2);
       int nblk = 0;
       for (int bi = 0; bi < ga.nbi; ++bi) nblk += ga.nbj - bi;
@@ -938,7 +1063,7 @@ kvx_status kvx_fit_query(kvx_fit* f, kvx_fit_info* info) {
   *info = kvx_fit_info{};
   info->systems = 2 * f->tgt.n_layers;
   info->n = f->n;
-  const int nbi = f->din_p / kFB, nbj = f->F / kFB;
+  const int nbi = f->din_z / kFB, nbj = f->F2 / kFB;
   for (int bi = 0; bi < nbi; ++bi) info->gram_blocks += nbj - bi;
   info->rows = f->rows;
   info->device_bytes = static_cast<int64_t>(size_t(f->tgt.n_layers) * 2 * f->din_p * f->F *

@@ -211,3 +211,38 @@ def test_fitted_weights_translate():
     print(f"[fit] end-to-end K relative distance {rel:.3e}", flush=True)
     assert rel <= 3e-2
     dev.close()
+
+
+def test_fit_full_size_qwen_4k_all_layers():
+    """The benchmark's fit workload at full size: Qwen2.5-7B -> 1.5B geometry,
+    4096 rows, all 28 target layers, K and V (Section 5's distance with a
+    ridge).  Every layer's W against the fp64 oracle's, and every layer's
+    objective against the oracle's optimum."""
+    lam = 1.0
+    spec = S.config(2)
+    prob = S.make_problem(spec)
+    tk, tv = _native(prob, noise=0.1)
+    print("[fit] full size qwen 4k", flush=True)
+    got, rows = _gpu_fit(prob, tk, tv, lam=lam)
+    assert rows == 4096
+    ref = F.fit(prob, tk, tv, lam, True)
+    for which, tgt in ((0, tk), (1, tv)):
+        Y = F.target_rows(prob, tgt, which)
+        worst_rel, worst_obj = 0.0, 0.0
+        for l in range(spec.tgt.n_layers):
+            gw, gb = got[which][l], got[2 + which][l]
+            rw, rb = ref[which][l], ref[2 + which][l]
+            assert np.isfinite(gw).all() and np.isfinite(gb).all()
+            rel = np.linalg.norm(gw - rw) / np.linalg.norm(rw)
+            assert rel <= 1e-3, f"layer {l} {'KV'[which]}: W relative error {rel:.3e}"
+            Z = F.source_rows(prob, l, which)
+
+            def obj(w, b):
+                r = Y[l] - Z @ w.T - b
+                return float((r * r).sum()) + lam * float((w * w).sum())
+
+            jo, jr = obj(gw, gb), obj(rw, rb)
+            assert jo <= jr * (1 + 1e-5), f"layer {l} {'KV'[which]}: {jo:.9e} vs {jr:.9e}"
+            worst_rel, worst_obj = max(worst_rel, rel), max(worst_obj, jo / jr - 1)
+        print(f"[fit] full size {'KV'[which]}: worst W rel err {worst_rel:.2e}, "
+              f"worst objective excess {worst_obj:.2e}", flush=True)
