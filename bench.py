@@ -504,6 +504,26 @@ def fit_flops(spec, rows: int, fit_bias: bool = True) -> int:
     return 2 * spec.tgt.n_layers * 2 * rows * (n * (n + 1) // 2 + n * spec.d_out)
 
 
+def fit_issued_flops(spec, prob, rows: int) -> int:
+    """Matrix-core flops fit_gram issues for `rows` rows: 128 x 128 blocks
+    (bi over the Z features, bj >= bi over Z and Y, padded), rows padded to
+    64, and per block the products hi*hi (+ hi*lo, lo*hi for operands that are
+    not exact bf16: computed ones, or fp32 data)."""
+    bf = spec.dtype == "bf16"
+    ident = prob.row_ptr is None
+    nbz = -(-spec.d_in // 128)
+    nbj = nbz + -(-spec.d_out // 128)
+    rows_p = -(-rows // 64) * 64
+    total = 0
+    for kv in (0, 1):
+        lo_z = not (bf and ident and (kv == 1 or spec.src.rope_base <= 0))
+        lo_y = not (bf and (kv == 1 or spec.tgt.rope_base <= 0))
+        for bi in range(nbz):
+            for bj in range(bi, nbj):
+                total += 1 + lo_z + (lo_z if bj < nbz else lo_y)
+    return 2 * 128 * 128 * rows_p * total * spec.tgt.n_layers
+
+
 def fit_cpu_baseline(spec, prob, tk, tv, lam: float, budget_s: float):
     """The fp64 fit oracle on the host over as many target layers as fit the
     budget (all rows, K and V), scaled to rows per second of the whole job."""
@@ -610,8 +630,7 @@ def main_fit(args, spec, prob, torch, kvx, S):
                      "traffic": None, "kernel": "fit_gram",
                      "flops_per_launch": int(flops_launch), "ms_per_launch": round(ms_gram, 5),
                      "issued_mfma_flops_per_launch": int(
-                         3 * 2 * 128 * 128 * info.gram_blocks * info.systems * 32 *
-                         ((rows + 31) // 32) / launches_per_step)},
+                         fit_issued_flops(spec, prob, rows) / launches_per_step)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -100,7 +100,7 @@ kvx_status kvx_fit_solve(kvx_fit* fit, double lambda, float* w_k, float* w_v, fl
  * device the library is loaded on holds until the process ends; systems are
  * solved in groups that fit it, in stream order.  Limit: one system's
  * (n^2 + n*dout) doubles, n = mix*Hs*Ds + fit_bias, must fit in the workspace
- * (n up to 3848 at dout 512), else KVX_EUNSUPPORTED with nothing
+ * (n up to 3840 at dout 512), else KVX_EUNSUPPORTED with nothing
  * enqueued.  The current device must be the fit's (KVX_EINVAL otherwise).
  * Every call on a device shares that device's workspace: calls that overlap
  * on one device (other streams, other threads) race and must be serialised

@@ -39,7 +39,6 @@ constexpr int kSlab = 32;      // rows per LDS slab of the Gram kernel
 constexpr int kPrepRows = 64;  // rows per workgroup of fit_prepare (rows padded to it)
 constexpr int kPitch = kSlab + 8;  // LDS pitch (bf16) of one feature's slab row
 constexpr int kFitBatch = 64;  // contexts per launch
-constexpr int kNB = 32;        // Cholesky panel width
 
 kvx_status fit_hip_fail(hipError_t e) { return hip_status(e); }
 
@@ -167,32 +166,77 @@ __global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
     const int g = lane % 8;
     const int npairs = isz ? a.din / 2 : a.dout / 2;
     const int p0 = 64 * (isz ? jt : jt - a.tz) + 8 * g;  // 8 pairs of one head
-#pragma unroll 1
-    for (int u = 0; u < 2; ++u) {
-      const int i = lane / 8 + 8 * w + 32 * u;
-      const int r = r0 + i;
-      float v1[8], v2[8];
+    const int half = (isz ? a.ds : a.dt) / 2;
+    const int hp = p0 / half, i0 = p0 % half;
+    const int j = hp / a.hs, hz = hp % a.hs;  // Z: mixed layer, source head
+    const T* zb = isz ? static_cast<const T*>(a.src[kv]) +
+                            a.layer_map[l * a.mix + (p0 < npairs ? j : 0)] * a.ss.l +
+                            hz * a.ss.h + i0
+                      : nullptr;
+    const T* yb = isz ? nullptr
+                      : static_cast<const T*>(a.tgt[kv]) + l * a.ts.l + hp * a.ts.h + i0;
+    const bool rot = kv == 0 && (isz ? a.src_rope : a.tgt_rope);
+    const double* fr = (isz ? a.fs : a.ft) + i0;
+    if (!isz || !a.row_ptr) {
+      // one row per unit (native target rows, identity-aligned source rows):
+      // both units' loads are issued before either is used
+      const T* ptr[2];
+      int pos[2];
+      bool ok[2];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) v1[q] = v2[q] = 0.f;
-      if (r < a.nrows && p0 < npairs) {
-        const int b = ctx_of(a.ctx, r);
-        const int t = r - a.ctx.row0[b];
-        if (isz) {
-          const int half = a.ds / 2;
-          const int jh = p0 / half, i0 = p0 % half;
-          const int j = jh / a.hs, h = jh % a.hs;
-          const int ls = a.layer_map[l * a.mix + j];
-          const T* sb = static_cast<const T*>(a.src[kv]) + ls * a.ss.l + b * a.ss.b +
-                        h * a.ss.h + i0;
-          const bool rot = kv == 0 && a.src_rope;
-          int e0 = 0, e1 = 1;
-          if (a.row_ptr) {
-            e0 = a.row_ptr[a.ctx.csr0[b] + t];
-            e1 = a.row_ptr[a.ctx.csr0[b] + t + 1];
+      for (int u = 0; u < 2; ++u) {
+        const int r = r0 + lane / 8 + 8 * w + 32 * u;
+        ok[u] = r < a.nrows && p0 < npairs;
+        const int b = ctx_of(a.ctx, ok[u] ? r : 0);
+        const int t = ok[u] ? r - a.ctx.row0[b] : 0;
+        pos[u] = t;
+        ptr[u] = isz ? zb + b * a.ss.b + t * a.ss.t : yb + b * a.ts.b + t * a.ts.t;
+      }
+      float x[2][2][8];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        if (ok[u]) {
+          load8<T>(ptr[u], vec, x[u][0]);
+          load8<T>(ptr[u] + half, vec, x[u][1]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) x[u][0][q] = x[u][1][q] = 0.f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int i = lane / 8 + 8 * w + 32 * u;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          float y1 = x[u][0][q], y2 = x[u][1][q];
+          if (rot) {
+            float c, sn;
+            rope_cs(fr[q], pos[u], c, sn);
+            y1 = x[u][0][q] * c + x[u][1][q] * sn;
+            y2 = x[u][1][q] * c - x[u][0][q] * sn;
           }
+          tr[8 * g + q][i] = y1;
+          tr[64 + 8 * g + q][i] = y2;
+        }
+      }
+    } else {
+      // pooled source rows (span alignment): entries of the CSR row
+#pragma unroll 1
+      for (int u = 0; u < 2; ++u) {
+        const int i = lane / 8 + 8 * w + 32 * u;
+        const int r = r0 + i;
+        float v1[8], v2[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v1[q] = v2[q] = 0.f;
+        if (r < a.nrows && p0 < npairs) {
+          const int b = ctx_of(a.ctx, r);
+          const int t = r - a.ctx.row0[b];
+          const T* sb = zb + b * a.ss.b;
+          const int e0 = a.row_ptr[a.ctx.csr0[b] + t];
+          const int e1 = a.row_ptr[a.ctx.csr0[b] + t + 1];
           for (int e = e0; e < e1; ++e) {
-            const int k = a.row_ptr ? a.col_idx[e] : t;
-            const float wt = a.row_ptr ? a.weight[e] : 1.f;
+            const int k = a.col_idx[e];
+            const float wt = a.weight[e];
             float x1[8], x2[8];
             load8<T>(sb + k * a.ss.t, vec, x1);
             load8<T>(sb + k * a.ss.t + half, vec, x2);
@@ -201,7 +245,7 @@ __global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
               float y1 = x1[q], y2 = x2[q];
               if (rot) {
                 float c, sn;
-                rope_cs(a.fs[i0 + q], k, c, sn);
+                rope_cs(fr[q], k, c, sn);
                 y1 = x1[q] * c + x2[q] * sn;
                 y2 = x2[q] * c - x1[q] * sn;
               }
@@ -209,30 +253,12 @@ __global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
               v2[q] += wt * y2;
             }
           }
-        } else {
-          const int half = a.dt / 2;
-          const int h = p0 / half, i0 = p0 % half;
-          const T* rowp = static_cast<const T*>(a.tgt[kv]) + l * a.ts.l + b * a.ts.b +
-                          h * a.ts.h + t * a.ts.t + i0;
-          load8<T>(rowp, vec, v1);
-          load8<T>(rowp + half, vec, v2);
-          if (kv == 0 && a.tgt_rope) {
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-              float c, sn;
-              rope_cs(a.ft[i0 + q], t, c, sn);
-              const float y1 = v1[q] * c + v2[q] * sn;
-              const float y2 = v2[q] * c - v1[q] * sn;
-              v1[q] = y1;
-              v2[q] = y2;
-            }
-          }
         }
-      }
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        tr[8 * g + q][i] = v1[q];
-        tr[64 + 8 * g + q][i] = v2[q];
+        for (int q = 0; q < 8; ++q) {
+          tr[8 * g + q][i] = v1[q];
+          tr[64 + 8 * g + q][i] = v2[q];
+        }
       }
     }
   } else {
@@ -429,203 +455,350 @@ struct SolveArgs {
   const float* acc;  // [sys][din_p][F]
   double* A;         // [group][n][n] workspace, one per system of the launch
   double* X;         // [group][n][dout] workspace (right-hand sides, then solution)
-  int32_t sys0;      // first system of the launch: block b solves system sys0 + b
+  int32_t sys0;      // first system of the launch: system sys0 + blockIdx.y (.x)
   float* w[2];       // [Lt][dout][din]
   float* b[2];       // [Lt][dout] or nullptr
   int32_t* status;   // set to 1 if a pivot is not positive
   double lam;
   int32_t n, din, dout, din_p, F, fit_bias;
+  int32_t np;  // n rounded up to the panel width: the padding unknowns get an
+               // identity block and zero right-hand sides (so they solve to 0)
 };
 
-// One workgroup per system (l, kv): blocked right-looking Cholesky of
-// A = Zt^T Zt + lam D in fp64, then L L^T X = Zt^T Y.
-__global__ void __launch_bounds__(256) fit_solve(SolveArgs a) {
-  __shared__ double pk[kNB][kNB + 1];   // diagonal block / factor
-  __shared__ double pr[kNB][kNB + 1];   // panel rows (tile i)
-  __shared__ double pc[kNB][kNB + 1];   // panel rows (tile j)
-  const int sys = a.sys0 + blockIdx.x;
-  const int tid = threadIdx.x;
-  const int n = a.n, m = a.dout;
-  const float* acc = a.acc + static_cast<int64_t>(sys) * a.din_p * a.F;
-  double* A = a.A + static_cast<int64_t>(blockIdx.x) * n * n;
-  double* X = a.X + static_cast<int64_t>(blockIdx.x) * n * m;
+// The solve of each (layer, K|V) system, A = Zt^T Zt + lam D and
+// L L^T X = Zt^T Y in fp64, as a blocked right-looking Cholesky spread over
+// many workgroups: per 32-wide panel, one workgroup per system factors the
+// diagonal block, solves the panel's rows below it and the panel's rows of
+// the forward substitution (L Y = B); then 64 x 64 tiles of the trailing
+// matrix and of the right-hand sides are updated by one workgroup each.  The
+// backward substitution (L^T X = Y) runs panel by panel from the last, again
+// with one workgroup per system for the diagonal block and tiles for the
+// updates of the rows above.
+constexpr int kSB = 32;  // panel width
+constexpr int kST = 64;  // update tile edge
 
-  // lower triangle of A from the upper accumulator blocks; ridge on Z only
-  for (int64_t idx = tid; idx < static_cast<int64_t>(n) * n; idx += 256) {
-    const int i = static_cast<int>(idx / n), j = static_cast<int>(idx % n);
-    if (j > i) continue;
-    double v = acc[static_cast<int64_t>(j) * a.F + i];
-    if (i == j && i < a.din) v += a.lam;
-    A[static_cast<int64_t>(i) * n + j] = v;
+__device__ __forceinline__ double* sys_A(const SolveArgs& a, int g) {
+  return a.A + static_cast<int64_t>(g) * a.np * a.np;
+}
+__device__ __forceinline__ double* sys_X(const SolveArgs& a, int g) {
+  return a.X + static_cast<int64_t>(g) * a.np * a.dout;
+}
+
+// Lower triangle of A (ridge on the din weight unknowns, not the bias) and
+// X = Zt^T Y from the upper accumulator blocks.  grid: (chunks, systems).
+__global__ void __launch_bounds__(256) solve_build(SolveArgs a) {
+  const int g = blockIdx.y;
+  const float* acc = a.acc + static_cast<int64_t>(a.sys0 + g) * a.din_p * a.F;
+  double* A = sys_A(a, g);
+  double* X = sys_X(a, g);
+  const int np = a.np;
+  const int64_t nn = static_cast<int64_t>(np) * np;
+  const int64_t total = nn + static_cast<int64_t>(np) * a.dout;
+  for (int64_t idx = blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += static_cast<int64_t>(gridDim.x) * 256) {
+    if (idx < nn) {
+      const int i = static_cast<int>(idx / np), j = static_cast<int>(idx % np);
+      double v = 0.0;
+      if (i >= a.n || j >= a.n) {
+        v = i == j ? 1.0 : 0.0;
+      } else if (j <= i) {
+        v = acc[static_cast<int64_t>(j) * a.F + i];
+        if (i == j && i < a.din) v += a.lam;
+      }
+      A[idx] = v;
+    } else {
+      const int64_t k = idx - nn;
+      const int i = static_cast<int>(k / a.dout), c = static_cast<int>(k % a.dout);
+      X[k] = i < a.n ? acc[static_cast<int64_t>(i) * a.F + a.din_p + c] : 0.0;
+    }
   }
-  for (int64_t idx = tid; idx < static_cast<int64_t>(n) * m; idx += 256) {
-    const int i = static_cast<int>(idx / m), c = static_cast<int>(idx % m);
-    X[idx] = acc[static_cast<int64_t>(i) * a.F + a.din_p + c];
+}
+
+// Panel kb: factor the diagonal block in LDS and write L_kk back.
+// grid: (systems).
+__global__ void __launch_bounds__(256) solve_panel(SolveArgs a, int kb) {
+  __shared__ double pk[kSB][kSB + 1];
+  const int g = blockIdx.x, tid = threadIdx.x;
+  const int n = a.np;
+  constexpr int kw = kSB;
+  double* A = sys_A(a, g);
+  for (int idx = tid; idx < kSB * kSB; idx += 256) {
+    const int i = idx / kSB, j = idx % kSB;
+    pk[i][j] = (i < kw && j <= i) ? A[static_cast<int64_t>(kb + i) * n + kb + j] : 0.0;
   }
   __syncthreads();
-
   bool bad = false;
-  for (int kb = 0; kb < n; kb += kNB) {
-    const int kw = min(kNB, n - kb);
-    // (1) factor the diagonal block in LDS
-    for (int idx = tid; idx < kNB * kNB; idx += 256) {
-      const int i = idx / kNB, j = idx % kNB;
-      pk[i][j] = (i < kw && j <= i) ? A[static_cast<int64_t>(kb + i) * n + kb + j] : 0.0;
+  for (int k = 0; k < kw; ++k) {
+    const double dkk = pk[k][k];
+    const bool ok = dkk > 0.0 && isfinite(dkk);
+    bad |= !ok;
+    const double d = ok ? sqrt(dkk) : 1.0;
+    __syncthreads();
+    if (tid == 0) pk[k][k] = d;
+    for (int i = k + 1 + tid; i < kw; i += 256) pk[i][k] /= d;
+    __syncthreads();
+    for (int idx = tid; idx < kSB * kSB; idx += 256) {
+      const int i = idx / kSB, j = idx % kSB;
+      if (i > k && j > k && j <= i && i < kw) pk[i][j] -= pk[i][k] * pk[j][k];
     }
     __syncthreads();
-    for (int k = 0; k < kw; ++k) {
-      const double dkk = pk[k][k];
-      const bool ok = dkk > 0.0 && isfinite(dkk);
-      bad |= !ok;
-      const double d = ok ? sqrt(dkk) : 1.0;
-      __syncthreads();
-      if (tid == 0) pk[k][k] = d;
-      for (int i = k + 1 + tid; i < kw; i += 256) pk[i][k] /= d;
-      __syncthreads();
-      for (int idx = tid; idx < kNB * kNB; idx += 256) {
-        const int i = idx / kNB, j = idx % kNB;
-        if (i > k && j > k && j <= i && i < kw) pk[i][j] -= pk[i][k] * pk[j][k];
-      }
-      __syncthreads();
-    }
-    for (int idx = tid; idx < kNB * kNB; idx += 256) {
-      const int i = idx / kNB, j = idx % kNB;
-      if (i < kw && j <= i) A[static_cast<int64_t>(kb + i) * n + kb + j] = pk[i][j];
-    }
-    // (2) panel below: row i solves x L_kk^T = a_i (forward substitution)
-    for (int i = kb + kw + tid; i < n; i += 256) {
-      double* row = A + static_cast<int64_t>(i) * n + kb;
-      for (int q = 0; q < kw; ++q) {
-        double s = row[q];
-        for (int p = 0; p < q; ++p) s -= row[p] * pk[q][p];
-        row[q] = s / pk[q][q];
-      }
-    }
-    __syncthreads();
-    // (3) trailing update of the lower triangle, 32 x 32 tiles
-    const int t0 = kb + kw;
-    const int nt = (n - t0 + kNB - 1) / kNB;
-    for (int ti = 0; ti < nt; ++ti) {
-      for (int tj = 0; tj <= ti; ++tj) {
-        const int i0 = t0 + ti * kNB, j0 = t0 + tj * kNB;
-        for (int idx = tid; idx < kNB * kNB; idx += 256) {
-          const int r = idx / kNB, q = idx % kNB;
-          pr[r][q] = (i0 + r < n && q < kw) ? A[static_cast<int64_t>(i0 + r) * n + kb + q] : 0.0;
-          pc[r][q] = (j0 + r < n && q < kw) ? A[static_cast<int64_t>(j0 + r) * n + kb + q] : 0.0;
-        }
-        __syncthreads();
-        for (int idx = tid; idx < kNB * kNB; idx += 256) {
-          const int r = idx / kNB, c = idx % kNB;
-          const int i = i0 + r, j = j0 + c;
-          if (i < n && j < n && j <= i) {
-            double s = 0.0;
-            for (int q = 0; q < kw; ++q) s += pr[r][q] * pc[c][q];
-            A[static_cast<int64_t>(i) * n + j] -= s;
-          }
-        }
-        __syncthreads();
-      }
-    }
   }
-  if (bad) a.status[0] = 1;
-  __syncthreads();
+  if (bad && tid == 0) a.status[0] = 1;
+  for (int idx = tid; idx < kSB * kSB; idx += 256) {
+    const int i = idx / kSB, j = idx % kSB;
+    if (i < kw && j <= i) A[static_cast<int64_t>(kb + i) * n + kb + j] = pk[i][j];
+  }
+}
 
-  // L Y = B, then L^T X = Y, blocked: each thread owns one right-hand side
-  // column (chunks of 256 columns); the 32 unknowns of the current block
-  // live in registers and the L tiles they need are staged in LDS.
-  for (int c0 = 0; c0 < m; c0 += 256) {
-    const int c = c0 + tid;
-    const bool on = c < m;
-    double y[kNB];
-    // forward
-    for (int kb = 0; kb < n; kb += kNB) {
-      const int kw = min(kNB, n - kb);
-      for (int idx = tid; idx < kNB * kNB; idx += 256) {
-        const int i = idx / kNB, j = idx % kNB;
-        pk[i][j] = (i < kw && j <= i) ? A[static_cast<int64_t>(kb + i) * n + kb + j] : 0.0;
-      }
-      __syncthreads();
-#pragma unroll
-      for (int q = 0; q < kNB; ++q) {
-        double v = 0.0;
-        if (on && q < kw) {
-          v = X[static_cast<int64_t>(kb + q) * m + c];
-#pragma unroll
-          for (int p = 0; p < q; ++p) v -= pk[q][p] * y[p];
-          v /= pk[q][q];
-          X[static_cast<int64_t>(kb + q) * m + c] = v;
-        }
-        y[q] = v;
-      }
-      for (int i0 = kb + kw; i0 < n; i0 += kNB) {
-        __syncthreads();
-        for (int idx = tid; idx < kNB * kNB; idx += 256) {
-          const int r = idx / kNB, q = idx % kNB;
-          pr[r][q] = (i0 + r < n && q < kw) ? A[static_cast<int64_t>(i0 + r) * n + kb + q] : 0.0;
-        }
-        __syncthreads();
-        if (on)
-          for (int r = 0; r < kNB && i0 + r < n; ++r) {
-            double v = X[static_cast<int64_t>(i0 + r) * m + c];
-#pragma unroll
-            for (int q = 0; q < kNB; ++q) v -= pr[r][q] * y[q];
-            X[static_cast<int64_t>(i0 + r) * m + c] = v;
-          }
-      }
-      __syncthreads();
-    }
-    // backward
-    const int nblk = (n + kNB - 1) / kNB;
-    for (int bk = nblk - 1; bk >= 0; --bk) {
-      const int kb = bk * kNB;
-      const int kw = min(kNB, n - kb);
-      for (int idx = tid; idx < kNB * kNB; idx += 256) {
-        const int i = idx / kNB, j = idx % kNB;
-        pk[i][j] = (i < kw && j <= i) ? A[static_cast<int64_t>(kb + i) * n + kb + j] : 0.0;
-      }
-      __syncthreads();
-#pragma unroll
-      for (int q = kNB - 1; q >= 0; --q) {
-        double v = 0.0;
-        if (on && q < kw) {
-          v = X[static_cast<int64_t>(kb + q) * m + c];
-#pragma unroll
-          for (int p = q + 1; p < kNB; ++p) v -= (p < kw ? pk[p][q] * y[p] : 0.0);
-          v /= pk[q][q];
-          X[static_cast<int64_t>(kb + q) * m + c] = v;
-        }
-        y[q] = v;
-      }
-      // rows above: X[i] -= sum_q L[kb + q][i] x_q
-      for (int i0 = 0; i0 < kb; i0 += kNB) {
-        __syncthreads();
-        for (int idx = tid; idx < kNB * kNB; idx += 256) {
-          const int q = idx / kNB, r = idx % kNB;
-          pr[r][q] = q < kw ? A[static_cast<int64_t>(kb + q) * n + i0 + r] : 0.0;
-        }
-        __syncthreads();
-        if (on)
-          for (int r = 0; r < kNB; ++r) {
-            double v = X[static_cast<int64_t>(i0 + r) * m + c];
-#pragma unroll
-            for (int q = 0; q < kNB; ++q) v -= pr[r][q] * y[q];
-            X[static_cast<int64_t>(i0 + r) * m + c] = v;
-          }
-      }
-      __syncthreads();
-    }
+// Panel kb, after its factor, `rhs` false: each thread one row below the
+// diagonal block, L[i][kb..] = A[i][kb..] L_kk^-T; `rhs` true: each thread
+// one right-hand side column of the panel's rows of L Y = B (X_k already
+// holds B_k minus the earlier panels' terms).  Separate instantiations, so
+// the compiler does not keep the factor's values live across both.
+// grid: (ceil(items / 256), systems).
+template <bool RHS>
+__global__ void __launch_bounds__(256) solve_panel_rows(SolveArgs a, int kb) {
+  __shared__ double pk[kSB][kSB + 1];
+  const int g = blockIdx.y, tid = threadIdx.x;
+  const int n = a.np, m = a.dout;
+  constexpr int kw = kSB;
+  double* A = sys_A(a, g);
+  double* X = sys_X(a, g);
+  for (int idx = tid; idx < kSB * kSB; idx += 256) {
+    const int i = idx / kSB, j = idx % kSB;
+    pk[i][j] = (i < kw && j <= i) ? A[static_cast<int64_t>(kb + i) * n + kb + j]
+                                  : (i == j ? 1.0 : 0.0);
   }
   __syncthreads();
-  const int l = sys / 2, kv = sys % 2;
+  const int item = blockIdx.x * 256 + tid;
+  if (item >= (RHS ? m : n - kb - kw)) return;
+  double* base = RHS ? X + static_cast<int64_t>(kb) * m + item
+                     : A + static_cast<int64_t>(kb + kw + item) * n + kb;
+  const int64_t step = RHS ? m : 1;
+  double r[kSB];
+#pragma unroll
+  for (int q = 0; q < kSB; ++q) r[q] = q < kw ? base[q * step] : 0.0;
+  // column by column: r_q is final once the earlier columns are subtracted
+#pragma unroll
+  for (int q = 0; q < kSB; ++q) {
+    r[q] /= pk[q][q];
+#pragma unroll
+    for (int p = q + 1; p < kSB; ++p) r[p] -= pk[p][q] * r[q];
+  }
+#pragma unroll
+  for (int q = 0; q < kSB; ++q)
+    if (q < kw) base[q * step] = r[q];
+}
+
+// Trailing update after panel kb: 64 x 64 tiles of the lower triangle of
+// A[t0:, t0:] (A[i][j] -= sum_q L[i][kb+q] L[j][kb+q]) and of X[t0:, :]
+// (X[i][c] -= sum_q L[i][kb+q] Y[kb+q][c]), t0 = kb + 32.  Thread: a 4 x 4
+// block of the tile.  grid: (tiles, systems).
+__global__ void __launch_bounds__(256) solve_update(SolveArgs a, int kb) {
+  __shared__ double P[kST][kSB + 1];  // L rows of the tile's rows
+  __shared__ double Q[kST][kSB + 1];  // L rows of the tile's columns, or Y_k transposed
+  const int g = blockIdx.y, tid = threadIdx.x;
+  const int n = a.np, m = a.dout;
+  constexpr int kw = kSB;
+  const int t0 = kb + kw;
+  const int nt = (n - t0 + kST - 1) / kST;
+  const int ntri = nt * (nt + 1) / 2;
+  const int nct = (m + kST - 1) / kST;
+  int tile = blockIdx.x;
+  if (tile >= ntri + nt * nct) return;
+  double* A = sys_A(a, g);
+  double* X = sys_X(a, g);
+  const bool onA = tile < ntri;
+  int ti, tj;
+  if (onA) {
+    ti = 0;
+    while ((ti + 1) * (ti + 2) / 2 <= tile) ++ti;
+    tj = tile - ti * (ti + 1) / 2;
+  } else {
+    tile -= ntri;
+    ti = tile / nct;
+    tj = tile % nct;
+  }
+  const int i0 = t0 + ti * kST;
+  const int j0 = onA ? t0 + tj * kST : tj * kST;
+  for (int idx = tid; idx < kST * kSB; idx += 256) {
+    const int r = idx / kSB, q = idx % kSB;
+    P[r][q] = (i0 + r < n && q < kw) ? A[static_cast<int64_t>(i0 + r) * n + kb + q] : 0.0;
+    if (onA)
+      Q[r][q] = (j0 + r < n && q < kw) ? A[static_cast<int64_t>(j0 + r) * n + kb + q] : 0.0;
+    else  // Q[c][q] = Y[kb + q][j0 + c]
+      Q[r][q] = (j0 + r < m && q < kw) ? X[static_cast<int64_t>(kb + q) * m + j0 + r] : 0.0;
+  }
+  __syncthreads();
+  const int rb = (tid / 16) * 4, cb = (tid % 16) * 4;
+  double s[4][4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) s[x][y] = 0.0;
+#pragma unroll 4
+  for (int q = 0; q < kw; ++q) {
+    double pv[4], qv[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      pv[x] = P[rb + x][q];
+      qv[x] = Q[cb + x][q];
+    }
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+      for (int y = 0; y < 4; ++y) s[x][y] += pv[x] * qv[y];
+  }
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) {
+      const int i = i0 + rb + x, j = j0 + cb + y;
+      if (onA) {
+        if (i < n && j <= i) A[static_cast<int64_t>(i) * n + j] -= s[x][y];
+      } else if (i < n && j < m) {
+        X[static_cast<int64_t>(i) * m + j] -= s[x][y];
+      }
+    }
+}
+
+// Backward substitution, panel kb (from the last): L_kk^T X_k = X_k, one
+// right-hand side column per thread.  grid: (ceil(dout / 256), systems).
+__global__ void __launch_bounds__(256) solve_back_diag(SolveArgs a, int kb) {
+  __shared__ double pk[kSB][kSB + 1];
+  const int g = blockIdx.y, tid = threadIdx.x;
+  const int n = a.np, m = a.dout;
+  constexpr int kw = kSB;
+  const double* A = sys_A(a, g);
+  double* X = sys_X(a, g);
+  for (int idx = tid; idx < kSB * kSB; idx += 256) {
+    const int i = idx / kSB, j = idx % kSB;
+    pk[i][j] = (i < kw && j <= i) ? A[static_cast<int64_t>(kb + i) * n + kb + j]
+                                  : (i == j ? 1.0 : 0.0);
+  }
+  __syncthreads();
+  const int c = blockIdx.x * 256 + tid;
+  if (c >= m) return;
+  double x[kSB];
+#pragma unroll
+  for (int q = 0; q < kSB; ++q) x[q] = q < kw ? X[static_cast<int64_t>(kb + q) * m + c] : 0.0;
+#pragma unroll
+  for (int q = kSB - 1; q >= 0; --q) {
+    double v = x[q];
+#pragma unroll
+    for (int p = q + 1; p < kSB; ++p) v -= pk[p][q] * x[p];
+    x[q] = v / pk[q][q];
+  }
+#pragma unroll
+  for (int q = 0; q < kSB; ++q)
+    if (q < kw) X[static_cast<int64_t>(kb + q) * m + c] = x[q];
+}
+
+// Backward update after panel kb: rows above it, X[j][c] -= sum_q
+// L[kb+q][j] X[kb+q][c] for j < kb, in 64 x 64 tiles.  grid: (tiles, systems).
+__global__ void __launch_bounds__(256) solve_back_update(SolveArgs a, int kb) {
+  __shared__ double P[kST][kSB + 1];  // P[r][q] = L[kb + q][j0 + r]
+  __shared__ double Q[kST][kSB + 1];  // Q[c][q] = X[kb + q][c0 + c]
+  const int g = blockIdx.y, tid = threadIdx.x;
+  const int n = a.np, m = a.dout;
+  constexpr int kw = kSB;
+  const int nct = (m + kST - 1) / kST;
+  const int nrt = (kb + kST - 1) / kST;
+  if (static_cast<int>(blockIdx.x) >= nrt * nct) return;
+  const double* A = sys_A(a, g);
+  double* X = sys_X(a, g);
+  const int j0 = (blockIdx.x / nct) * kST, c0 = (blockIdx.x % nct) * kST;
+  for (int idx = tid; idx < kST * kSB; idx += 256) {
+    const int q = idx / kST, r = idx % kST;
+    P[r][q] = (q < kw && j0 + r < kb) ? A[static_cast<int64_t>(kb + q) * n + j0 + r] : 0.0;
+    Q[r][q] = (q < kw && c0 + r < m) ? X[static_cast<int64_t>(kb + q) * m + c0 + r] : 0.0;
+  }
+  __syncthreads();
+  const int rb = (tid / 16) * 4, cb = (tid % 16) * 4;
+  double s[4][4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) s[x][y] = 0.0;
+#pragma unroll 4
+  for (int q = 0; q < kw; ++q) {
+    double pv[4], qv[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      pv[x] = P[rb + x][q];
+      qv[x] = Q[cb + x][q];
+    }
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+      for (int y = 0; y < 4; ++y) s[x][y] += pv[x] * qv[y];
+  }
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) {
+      const int j = j0 + rb + x, c = c0 + cb + y;
+      if (j < kb && c < m) X[static_cast<int64_t>(j) * m + c] -= s[x][y];
+    }
+}
+
+// W = X[:din]^T (nn.Linear order) and b = X[din].  grid: (chunks, systems).
+__global__ void __launch_bounds__(256) solve_write(SolveArgs a) {
+  const int g = blockIdx.y;
+  const int sys = a.sys0 + g;
+  const int l = sys / 2, kv = sys % 2, m = a.dout;
+  const double* X = sys_X(a, g);
   float* w = a.w[kv] + static_cast<int64_t>(l) * m * a.din;
-  for (int64_t idx = tid; idx < static_cast<int64_t>(m) * a.din; idx += 256) {
+  const int64_t total = static_cast<int64_t>(m) * a.din;
+  for (int64_t idx = blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += static_cast<int64_t>(gridDim.x) * 256) {
     const int c = static_cast<int>(idx / a.din), i = static_cast<int>(idx % a.din);
     w[idx] = static_cast<float>(X[static_cast<int64_t>(i) * m + c]);
   }
-  if (a.b[kv])
-    for (int c = tid; c < m; c += 256)
+  if (a.b[kv] && blockIdx.x == 0)
+    for (int c = threadIdx.x; c < m; c += 256)
       a.b[kv][static_cast<int64_t>(l) * m + c] =
           a.fit_bias ? static_cast<float>(X[static_cast<int64_t>(a.din) * m + c]) : 0.f;
+}
+
+// Enqueue the solve of `ng` systems (sa.sys0 ..) whose workspaces start at
+// sa.A and sa.X.
+kvx_status enqueue_solve(const SolveArgs& sa, int ng, hipStream_t st) {
+  const int n = sa.np, m = sa.dout;
+  const unsigned chunks = static_cast<unsigned>(
+      std::min<int64_t>(1024, (int64_t(n) * (n + m) + 2047) / 2048));
+  solve_build<<<dim3(chunks, ng), dim3(256), 0, st>>>(sa);
+  FIT_HIP(hipGetLastError());
+  const int nct = (m + kST - 1) / kST;
+  for (int kb = 0; kb < n; kb += kSB) {
+    solve_panel<<<dim3(ng), dim3(256), 0, st>>>(sa, kb);
+    FIT_HIP(hipGetLastError());
+    const int t0 = kb + std::min(kSB, n - kb);
+    if (t0 < n) {
+      solve_panel_rows<false><<<dim3((n - t0 + 255) / 256, ng), dim3(256), 0, st>>>(sa, kb);
+      FIT_HIP(hipGetLastError());
+    }
+    solve_panel_rows<true><<<dim3((m + 255) / 256, ng), dim3(256), 0, st>>>(sa, kb);
+    FIT_HIP(hipGetLastError());
+    if (t0 < n) {
+      const int nt = (n - t0 + kST - 1) / kST;
+      solve_update<<<dim3(nt * (nt + 1) / 2 + nt * nct, ng), dim3(256), 0, st>>>(sa, kb);
+      FIT_HIP(hipGetLastError());
+    }
+  }
+  for (int kb = (n - 1) / kSB * kSB; kb >= 0; kb -= kSB) {
+    solve_back_diag<<<dim3((m + 255) / 256, ng), dim3(256), 0, st>>>(sa, kb);
+    FIT_HIP(hipGetLastError());
+    if (kb > 0) {
+      solve_back_update<<<dim3(((kb + kST - 1) / kST) * nct, ng), dim3(256), 0, st>>>(sa, kb);
+      FIT_HIP(hipGetLastError());
+    }
+  }
+  const unsigned wchunks = static_cast<unsigned>(
+      std::min<int64_t>(256, (int64_t(m) * sa.din + 2047) / 2048));
+  solve_write<<<dim3(std::max(1u, wchunks), ng), dim3(256), 0, st>>>(sa);
+  FIT_HIP(hipGetLastError());
+  return KVX_OK;
 }
 
 // Status flag of a solve: cleared by a kernel (not a memset) before the
@@ -958,8 +1131,9 @@ kvx_status kvx_fit_solve(kvx_fit* f, double lambda, float* w_k, float* w_v, floa
   if (f->fit_bias && (!b_k || !b_v)) return KVX_EINVAL;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t nsys = int64_t(f->tgt.n_layers) * 2;
-  const size_t abytes = size_t(nsys) * f->n * f->n * sizeof(double);
-  const size_t xbytes = size_t(nsys) * f->n * f->dout * sizeof(double);
+  const int32_t np = static_cast<int32_t>(round_up(f->n, kSB));
+  const size_t abytes = size_t(nsys) * np * np * sizeof(double);
+  const size_t xbytes = size_t(nsys) * np * f->dout * sizeof(double);
   const size_t need = abytes + xbytes + 256;
   if (need > f->solve_bytes) {
     if (f->solve_buf) {
@@ -992,8 +1166,9 @@ kvx_status kvx_fit_solve(kvx_fit* f, double lambda, float* w_k, float* w_v, floa
   sa.din_p = f->din_p;
   sa.F = f->F;
   sa.fit_bias = f->fit_bias;
-  fit_solve<<<dim3(static_cast<unsigned>(nsys)), dim3(256), 0, st>>>(sa);
-  FIT_HIP(hipGetLastError());
+  sa.np = np;
+  const kvx_status es = enqueue_solve(sa, static_cast<int>(nsys), st);
+  if (es != KVX_OK) return es;
   int32_t h = 0;
   FIT_HIP(hipMemcpyAsync(&h, status, sizeof h, hipMemcpyDeviceToHost, st));
   FIT_HIP(hipStreamSynchronize(st));
@@ -1007,7 +1182,8 @@ kvx_status kvx_fit_solve_noalloc(kvx_fit* f, double lambda, float* w_k, float* w
   int dev = 0;
   FIT_HIP(hipGetDevice(&dev));
   if (dev != f->device) return KVX_EINVAL;
-  const size_t per_sys = (size_t(f->n) * f->n + size_t(f->n) * f->dout) * sizeof(double);
+  const int32_t np = static_cast<int32_t>(round_up(f->n, kSB));
+  const size_t per_sys = (size_t(np) * np + size_t(np) * f->dout) * sizeof(double);
   const int64_t group = int64_t((kSolveWorkspaceBytes - kStatusBytes) / per_sys);
   if (group < 1) return KVX_EUNSUPPORTED;
   void* ws = nullptr;
@@ -1023,7 +1199,7 @@ kvx_status kvx_fit_solve_noalloc(kvx_fit* f, double lambda, float* w_k, float* w
   SolveArgs sa{};
   sa.acc = f->acc;
   sa.A = reinterpret_cast<double*>(base);
-  sa.X = reinterpret_cast<double*>(base + size_t(g) * f->n * f->n * sizeof(double));
+  sa.X = reinterpret_cast<double*>(base + size_t(g) * np * np * sizeof(double));
   sa.w[0] = w_k;
   sa.w[1] = w_v;
   sa.b[0] = b_k;
@@ -1036,11 +1212,12 @@ kvx_status kvx_fit_solve_noalloc(kvx_fit* f, double lambda, float* w_k, float* w
   sa.din_p = f->din_p;
   sa.F = f->F;
   sa.fit_bias = f->fit_bias;
+  sa.np = np;
   // groups of systems in stream order reuse the same workspace
   for (int64_t s0 = 0; s0 < nsys; s0 += g) {
     sa.sys0 = static_cast<int32_t>(s0);
-    fit_solve<<<dim3(static_cast<unsigned>(std::min(g, nsys - s0))), dim3(256), 0, st>>>(sa);
-    FIT_HIP(hipGetLastError());
+    const kvx_status es = enqueue_solve(sa, static_cast<int>(std::min(g, nsys - s0)), st);
+    if (es != KVX_OK) return es;
   }
   int32_t h = 0;
   FIT_HIP(hipMemcpyAsync(&h, status, sizeof h, hipMemcpyDeviceToHost, st));
