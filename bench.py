@@ -109,6 +109,21 @@ def recorded_traffic(workload: str, precision: str, src_tokens: int, batch: int,
     return None if v is None else int(v)
 
 
+def gpu_clock_mhz():
+    """The shader clock the driver reports as current (sysfs `pp_dpm_sclk`,
+    the level marked `*`), sampled once while the timed calls run; None where
+    the file is not readable.  A sample, not an average over the run."""
+    for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            with open(path) as fh:
+                for line in fh:
+                    if line.strip().endswith("*"):
+                        return int(line.split(":")[1].strip().split("Mhz")[0].split("MHz")[0])
+        except (OSError, ValueError, IndexError):
+            continue
+    return None
+
+
 def cpu_baseline(spec, prob, budget_s: float):
     """Time the fp64 oracle on the host: all target layers of a bounded
     number of tokens, scaled to source tokens per second."""
@@ -294,10 +309,12 @@ def main():
         evs[i][0].record(stream)
         step(i)
         evs[i][1].record(stream)
+    clock = gpu_clock_mhz()  # sampled while the enqueued calls run
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall0
     ms_ev = evs[0][0].elapsed_time(evs[-1][1]) / args.steps
-    ms_kernel = sum(e0.elapsed_time(e1) for e0, e1 in evs) / args.steps
+    launch_ms = np.array([e0.elapsed_time(e1) for e0, e1 in evs])
+    ms_kernel = float(launch_ms.mean())
     ms_wall = t_wall * 1e3 / args.steps
     ms = max(ms_ev, 0.0)
 
@@ -365,6 +382,10 @@ def main():
                    "parallelism": "single GPU"},
         "ms_per_handoff": round(ms, 5) if spec.batch == 1 else None,
         "ms_wall_per_step": round(ms_wall, 5),
+        # spread of the per-launch durations (HIP events around each call)
+        "launch_ms_p10_p50_p90": [round(float(np.percentile(launch_ms, q)), 5)
+                                  for q in (10, 50, 90)],
+        "gpu_clock_mhz": clock,
         "roofline": roof,
         "cpu_baseline": cpu,
     }

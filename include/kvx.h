@@ -169,7 +169,11 @@ kvx_status kvx_plan_create(const kvx_plan_desc* desc, kvx_plan** out);
  * summing to 1 within n_row * 2^-23 -- pooling rows partition unity; any
  * violation returns KVX_EDATA with nothing enqueued).  batch == 0 or an
  * empty output is a no-op returning KVX_OK.  The plan is immutable and holds no
- * per-call scratch, so concurrent calls on different streams are safe. */
+ * per-call scratch, so concurrent calls on different streams are safe.
+ * Fault injection: with KVX_FAULT=launch in the environment a call that passes
+ * validation returns KVX_EHIP (kvx_last_hip_error() = hipErrorLaunchFailure)
+ * without enqueuing anything, so a caller's recovery path -- the fallback to
+ * native prefill when a translation is unavailable -- can be exercised. */
 kvx_status kvx_translate(const kvx_plan* plan, const kvx_io* io, void* stream);
 
 /* Translator variants, composed on the device into the plan's dense
@@ -257,7 +261,7 @@ kvx_status kvx_plan_query(const kvx_plan* plan, kvx_plan_info* info);
  *                      matrix cores;
  *   KVX_STAGE_STORE    bias, target RoPE on K, bf16 rounding, store into
  *                      the target cache (contiguous or paged).
- * Same arguments, layouts and validation as kvx_translate, for plans on the
+ * Same arguments, layouts, validation and fault injection as kvx_translate, for plans on the
  * fused kernel (bf16) with precision BF16X2, BF16 or BF16X2_OUTLIER (the
  * latter computed as BF16X2); other plans return KVX_EUNSUPPORTED, as do
  * buffers or strides that are not 16-byte aligned.

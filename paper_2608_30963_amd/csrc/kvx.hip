@@ -497,6 +497,15 @@ kvx_status validate_call(const Call& c, bool csr, bool blocks, hipStream_t st) {
   return KVX_OK;
 }
 
+// KVX_FAULT=launch: the call reports a failed launch (KVX_EHIP, with
+// hipErrorLaunchFailure for kvx_last_hip_error) after its validation, with
+// nothing enqueued -- so callers' recovery paths (the paper's fallback to
+// native prefill) can be tested without making a kernel fail.
+bool injected_launch_fault() {
+  const char* f = std::getenv("KVX_FAULT");
+  return f && std::strcmp(f, "launch") == 0;
+}
+
 // 16-byte vector access needs 16-byte aligned rows and buffers.
 bool rows_aligned16(const kvx_io& io, int esz) {
   for (int i = 0; i < 4; ++i)
@@ -520,6 +529,7 @@ extern "C" kvx_status kvx_translate(const kvx_plan* p, const kvx_io* io_in, void
   hipStream_t st = static_cast<hipStream_t>(stream);
   cs = validate_call(call, true, true, st);
   if (cs != KVX_OK) return cs;
+  if (injected_launch_fault()) return hip_fail(hipErrorLaunchFailure);
 
   const int esz = p->dtype == KVX_F32 ? 4 : 2;
   bool fused = p->kernel == kFused && rows_aligned16(io, esz);
@@ -710,6 +720,7 @@ extern "C" kvx_status kvx_translate_staged(const kvx_plan* p, const kvx_io* io_i
   hipStream_t st = static_cast<hipStream_t>(stream);
   s = validate_call(call, (stages & KVX_STAGE_POOL) != 0, (stages & KVX_STAGE_STORE) != 0, st);
   if (s != KVX_OK) return s;
+  if (injected_launch_fault()) return hip_fail(hipErrorLaunchFailure);
 
   StagedArgs a{};
   a.ss = Strides{io.src_stride[0], io.src_stride[1], io.src_stride[2], io.src_stride[3]};
