@@ -62,12 +62,13 @@ KERNEL_SOURCES = os.path.join(ROOT, "paper_2608_30963_amd", "csrc")
 
 
 def kernel_source_hash() -> str:
-    """sha256 over the translation's HIP sources (file names and contents,
-    sorted; the translator fit and the plan-time composition of translator
-    variants are not part of the translation launch)."""
+    """sha256 over the fused translation's HIP sources (file names and
+    contents, sorted; the translator fit, the plan-time composition of
+    translator variants and the staged path's separate kernels are not part
+    of the fused launch)."""
     h = hashlib.sha256()
     for f in sorted(glob.glob(os.path.join(KERNEL_SOURCES, "*"))):
-        if os.path.basename(f) in ("fit.hip", "compose.hip"):
+        if os.path.basename(f) in ("fit.hip", "compose.hip", "staged.hip", "staged.h"):
             continue
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:

@@ -36,13 +36,15 @@ def test_recorded_traffic_follows_the_kernel_sources(tmp_path, monkeypatch):
     assert look("qwen2.5-7b->qwen2.5-1.5b", "f16", 4096, 1, "contiguous") is None
     assert look("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 2048, 1, "contiguous") is None
     assert look("qwen2.5-7b->qwen2.5-1.5b", "bf16x2", 4096, 1, "paged16") is None
-    # a changed translation source invalidates it; the fit's source does not
+    # a changed fused-kernel source invalidates it; the fit's and the staged
+    # path's sources do not
     src = tmp_path / "csrc"
     shutil.copytree(bench.KERNEL_SOURCES, src)
     monkeypatch.setattr(bench, "KERNEL_SOURCES", str(src))
     h0 = bench.kernel_source_hash()
-    with open(src / "fit.hip", "a") as fh:
-        fh.write("\n// edit\n")
+    for other in ("fit.hip", "staged.hip", "staged.h"):
+        with open(src / other, "a") as fh:
+            fh.write("\n// edit\n")
     assert bench.kernel_source_hash() == h0
     with open(src / "kernel_mfma.h", "a") as fh:
         fh.write("\n// edit\n")
