@@ -3,7 +3,8 @@
 //   stage_pool     source RoPE removal on K and pooling over each target
 //                  row's alignment entries, in fp32, written as bf16 planes
 //                  hi (+ lo = the rounding residual) of the pooled inputs Z,
-//                  rows x din in the fused kernel's K-slot order;
+//                  rows x din (the fused kernel's K-slot order) stored in
+//                  matrix-core A-fragment order;
 //   stage_project  U = Z W^T per (target layer, K|V) on the matrix cores,
 //                  fp32 accumulation, against the plan's packed weights;
 //   stage_store    bias, target RoPE on K, bf16 rounding, store into the
@@ -33,8 +34,8 @@ struct StagedArgs {
   const int32_t* row_ptr;  // nullptr: identity alignment
   const int32_t* col_idx;
   const float* weight;
-  bf16_t* z;  // [nl][2 (K|V)][2 (hi|lo)][rows_p][din]
-  float* u;   // [nl][2 (K|V)][rows_p][dout]
+  bf16_t* z;  // [nl][2 (K|V)][2 (hi|lo)][rows_p / 32][din / 16][64 lanes][8]
+  float* u;   // [nl][2 (K|V)][rows_p / 32][dout / 32][16 registers][64 lanes]
   int32_t mix, hs, ds, ht, dt, din, dout;
   int32_t l0, nl;         // target layers of this launch: l0 .. l0 + nl - 1
   int32_t tiles, rows_p;  // row tiles of the launch's contexts, rows_p = tiles * 128

@@ -40,10 +40,32 @@ __device__ __forceinline__ void store_planes(bf16_t* hi, bf16_t* lo, bool two, c
   }
 }
 
+// Z is kept in the order stage_project's matrix-core loads read it: for
+// each block of 32 rows and each 16-slot K step, the 64 lanes' A fragments
+// (lane l: row l % 32, slots 8 (l / 32) .. +7) as one contiguous KiB, so a
+// wave's fragment load is one coalesced 1 KiB read.  Element offset of the 8
+// slots s .. s+7 (s % 8 == 0) of row r within one plane:
+__device__ __forceinline__ int64_t zfrag(int64_t r, int s, int ks_n) {
+  return (((r / 32) * ks_n + s / 16) * 64 + r % 32 + 32 * ((s / 8) % 2)) * 8;
+}
+
+// U (fp32, rows x dout) is kept in the order the MFMA accumulators hold it:
+// for each block of 32 rows and 32 outputs, register v (0..15) of the 64
+// lanes as 64 contiguous floats, lane l holding output l % 32 of row
+// 8 (v / 4) + 4 (l / 32) + v % 4.  The 32 outputs of a row stay contiguous.
+// Element offset of row r, output o:
+__device__ __forceinline__ int64_t ufrag(int64_t r, int o, int nb_n) {
+  const int rr = static_cast<int>(r % 32);
+  const int v = 4 * (rr / 8) + rr % 4, lane = o % 32 + 32 * ((rr / 4) % 2);
+  return (((r / 32) * nb_n + o / 32) * 16 + v) * 64 + lane;
+}
+
 // Stage 1.  grid: (row tiles, din / 128 chunks, layers x K|V); 256 threads.
 // Chunk c holds the RoPE pairs 64c .. 64c+63 of the flattened (mixed layer,
 // source head, frequency) list: first members in slots 0..63, second members
 // in 64..127.  Thread: one 8-pair group g of the chunk for rows tid/8 + 32u.
+// A wave's 64 stores cover 8 rows of 8 fragment slices each: 8 runs of
+// 128 contiguous bytes.
 __global__ void __launch_bounds__(256) stage_pool(StagedArgs a) {
   const int tile = blockIdx.x, c = blockIdx.y, sys = blockIdx.z;
   const int ll = sys / 2, kv = sys % 2, l = a.l0 + ll;
@@ -63,6 +85,10 @@ __global__ void __launch_bounds__(256) stage_pool(StagedArgs a) {
   const int64_t plane = static_cast<int64_t>(a.rows_p) * a.din;
   bf16_t* zb = a.z + static_cast<int64_t>(ll * 2 + kv) * 2 * plane;
   const bool two = a.planes[kv] == 2;
+  // fragment offset of slots c*128 + 8g of the thread's first row; the
+  // second members (slots + 64) sit 4 K steps further
+  const int64_t zu0 = zfrag(static_cast<int64_t>(tile) * kStageRows + threadIdx.x / 8,
+                            c * 128 + 8 * g, a.din / 16);
 #pragma unroll 1
   for (int u = 0; u < 4; ++u) {
     const int i = threadIdx.x / 8 + 32 * u;
@@ -98,94 +124,120 @@ __global__ void __launch_bounds__(256) stage_pool(StagedArgs a) {
         }
       }
     }
-    const int64_t row = static_cast<int64_t>(tile * kStageRows + i) * a.din + c * 128;
-    store_planes(zb + row + 8 * g, zb + plane + row + 8 * g, two, z1);
-    store_planes(zb + row + 64 + 8 * g, zb + plane + row + 64 + 8 * g, two, z2);
+    // rows i of this thread are i % 32 of row blocks 4 tile + u
+    bf16_t* zu = zb + zu0 + static_cast<int64_t>(u) * a.din * 32;
+    store_planes(zu, zu + plane, two, z1);
+    store_planes(zu + 4 * 512, zu + 4 * 512 + plane, two, z2);
   }
 }
 
-// Stage 2.  grid: (row tiles, 128-output tiles, layers x K|V); 4 waves, each
-// 64 rows x 64 outputs (2 x 2 tiles of v_mfma_f32_32x32x16_bf16).  Operand
-// fragments come straight from memory: Z rows (16 bytes per lane) and the
-// plan's packed weight fragments (1 KiB each); the next k-step's fragments
-// are loaded during the current one's MFMAs.
-__global__ void __launch_bounds__(256) stage_project(StagedArgs a) {
-  const int tile = blockIdx.x, nt = blockIdx.y, sys = blockIdx.z;
-  const int ll = sys / 2, kv = sys % 2, l = a.l0 + ll;
-  const int lane = threadIdx.x % 64, w = threadIdx.x / 64;
-  const int wi = w / 2, wj = w % 2;
-  const int nb_n = a.dout / 32, ks_n = a.din / 16;
-  const int nb0 = nt * 4 + wj * 2;  // first 32-output block of this wave
-  const int nbv = min(2, nb_n - nb0);
-  if (nbv <= 0) return;  // no barrier in this kernel
-  const int64_t plane = static_cast<int64_t>(a.rows_p) * a.din;
-  const bf16_t* zb = a.z + static_cast<int64_t>(ll * 2 + kv) * 2 * plane;
-  const bf16x8* wl = a.wp[kv] + static_cast<int64_t>(l) * nb_n * ks_n * 64;
-  const int r0 = tile * kStageRows + wi * 64;
-  const bool two = a.planes[kv] == 2;
-  f32x16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int jb = 0; jb < 2; ++jb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][jb][v] = 0.f;
-  // A fragment: lane l holds Z[row 32i + l%32][slot 16ks + 8(l/32) .. +7]
-  const bf16_t* zrow[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-    zrow[i] = zb + static_cast<int64_t>(r0 + 32 * i + lane % 32) * a.din + 8 * (lane / 32);
-  const bf16x8* wb[2];
-#pragma unroll
-  for (int jb = 0; jb < 2; ++jb)
-    wb[jb] = wl + static_cast<int64_t>(min(nb0 + jb, nb_n - 1)) * ks_n * 64 + lane;
+// Stage 2.  One work item: 128 rows x 256 outputs of one (target layer,
+// K|V) system, on 4 waves of 64 rows x 128 outputs (2 x 4 tiles of
+// v_mfma_f32_32x32x16_bf16).  Fragments come straight from memory as
+// contiguous KiB reads -- Z in fragment order, the plan's packed weights --
+// kPrefetch - 1 K steps ahead of the MFMAs that use them.  The 1-D grid is
+// laid out for the 8 XCDs: workgroup n runs on XCD n % 8, so n is mapped to
+// work item (n % 8) * per_xcd + n / 8 and each XCD walks one contiguous run
+// of items (system-major, then row tile, then output tile): the items
+// sharing a row tile, and the row tiles sharing a system's weights, run
+// together on one L2.
+constexpr int kProjRows = 128, kProjCols = 256, kPrefetch = 3;
+
+// The K steps of one wave's 64 x 128 tile; TWO: the operand has a lo plane.
+// Output blocks past dout (nbv < 4) are computed against the last block's
+// weights and not stored.
+template <bool TWO>
+__device__ __forceinline__ void project_steps(const bf16x8* const (&zrow)[2], int64_t plane8,
+                                              const bf16x8* const (&wb)[4], int ks_n,
+                                              f32x16 (&acc)[2][4]) {
   struct Frag {
-    bf16x8 A[2][2], B[2];
+    bf16x8 A[2][TWO ? 2 : 1], B[4];
   };
   auto load = [&](Frag& f, int ks) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      f.A[i][0] = *reinterpret_cast<const bf16x8*>(zrow[i] + ks * 16);
-      f.A[i][1] = two ? *reinterpret_cast<const bf16x8*>(zrow[i] + plane + ks * 16) : f.A[i][0];
+      f.A[i][0] = zrow[i][ks * 64];
+      if constexpr (TWO) f.A[i][1] = zrow[i][plane8 + ks * 64];
     }
 #pragma unroll
-    for (int jb = 0; jb < 2; ++jb) f.B[jb] = wb[jb][ks * 64];
+    for (int jb = 0; jb < 4; ++jb) f.B[jb] = wb[jb][ks * 64];
   };
   auto mma = [&](const Frag& f) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int jb = 0; jb < 2; ++jb)
-        if (jb < nbv) {
+      for (int jb = 0; jb < 4; ++jb) {
+        acc[i][jb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.A[i][0], f.B[jb], acc[i][jb], 0, 0, 0);
+        if constexpr (TWO)
           acc[i][jb] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.A[i][0], f.B[jb], acc[i][jb], 0, 0, 0);
-          if (two)
-            acc[i][jb] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.A[i][1], f.B[jb], acc[i][jb], 0, 0, 0);
-        }
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.A[i][1], f.B[jb], acc[i][jb], 0, 0, 0);
+      }
   };
-  Frag f0, f1;
-  load(f0, 0);
-  int ks = 0;
-  for (; ks + 2 <= ks_n; ks += 2) {
-    load(f1, ks + 1);
-    mma(f0);
-    if (ks + 2 < ks_n) load(f0, ks + 2);
-    mma(f1);
+  Frag f[kPrefetch];
+#pragma unroll
+  for (int s = 0; s + 1 < kPrefetch; ++s)
+    if (s < ks_n) load(f[s], s);
+  for (int k0 = 0; k0 < ks_n; k0 += kPrefetch) {
+#pragma unroll
+    for (int s = 0; s < kPrefetch; ++s) {
+      const int ks = k0 + s;
+      if (ks < ks_n) {
+        // refill the buffer the previous step consumed
+        if (ks + kPrefetch - 1 < ks_n) load(f[(s + kPrefetch - 1) % kPrefetch], ks + kPrefetch - 1);
+        mma(f[s]);
+      }
+    }
   }
-  if (ks < ks_n) mma(f0);
-  // D register v of lane l: row 8(v/4) + 4(l/32) + v%4, column l%32
+}
+
+__global__ void __launch_bounds__(256, 2) stage_project(StagedArgs a, int per_xcd) {
+  const int item = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
+  const int n_ct = (a.dout + kProjCols - 1) / kProjCols;
+  if (item >= a.nl * 2 * a.tiles * n_ct) return;  // no barrier in this kernel
+  const int ct = item % n_ct, tile = item / n_ct % a.tiles, sys = item / n_ct / a.tiles;
+  const int ll = sys / 2, kv = sys % 2, l = a.l0 + ll;
+  const int lane = threadIdx.x % 64, w = threadIdx.x / 64;
+  const int wi = w / 2, wj = w % 2;
+  const int nb_n = a.dout / 32, ks_n = a.din / 16;
+  const int nb0 = ct * (kProjCols / 32) + wj * 4;  // first 32-output block of this wave
+  const int nbv = min(4, nb_n - nb0);
+  if (nbv <= 0) return;
+  const int64_t plane = static_cast<int64_t>(a.rows_p) * a.din;
+  const bf16_t* zb = a.z + static_cast<int64_t>(ll * 2 + kv) * 2 * plane;
+  const bf16x8* wl = a.wp[kv] + static_cast<int64_t>(l) * nb_n * ks_n * 64;
+  const int r0 = tile * kProjRows + wi * 64;
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][jb][v] = 0.f;
+  // A fragment of row block i at K step ks: zrow[i][ks * 64], lo plane + plane8
+  const bf16x8* zrow[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+    zrow[i] =
+        reinterpret_cast<const bf16x8*>(zb + zfrag(r0 + 32 * i + lane % 32, 8 * (lane / 32), ks_n));
+  const bf16x8* wb[4];
+#pragma unroll
+  for (int jb = 0; jb < 4; ++jb)
+    wb[jb] = wl + static_cast<int64_t>(min(nb0 + jb, nb_n - 1)) * ks_n * 64 + lane;
+  if (a.planes[kv] == 2)
+    project_steps<true>(zrow, plane / 8, wb, ks_n, acc);
+  else
+    project_steps<false>(zrow, plane / 8, wb, ks_n, acc);
+  // U in D-fragment order: register v of every lane is 256 contiguous bytes
   float* ub = a.u + static_cast<int64_t>(ll * 2 + kv) * a.rows_p * a.dout;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int jb = 0; jb < 2; ++jb)
-      if (jb < nbv)
+    for (int jb = 0; jb < 4; ++jb)
+      if (jb < nbv) {
+        float* d = ub + ((static_cast<int64_t>(r0 / 32 + i) * nb_n + nb0 + jb) * 16) * 64 + lane;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int row = r0 + 32 * i + 8 * (v / 4) + 4 * (lane / 32) + v % 4;
-          ub[static_cast<int64_t>(row) * a.dout + (nb0 + jb) * 32 + lane % 32] = acc[i][jb][v];
-        }
+        for (int v = 0; v < 16; ++v) d[v * 64] = acc[i][jb][v];
+      }
 }
 
 // Stage 3.  grid: (32-row slices, groups of 8 threads' pair groups, layers x
@@ -205,14 +257,15 @@ __global__ void __launch_bounds__(256) stage_store(StagedArgs a) {
   const int h = q / gph, i0 = (q % gph) * 8;
   const int half = a.dt / 2;
   const int o1 = h * a.dt + i0, o2 = o1 + half;
-  const float* ur =
-      a.u + (static_cast<int64_t>(ll * 2 + kv) * a.rows_p + tile * kStageRows + i) * a.dout;
+  const float* ub = a.u + static_cast<int64_t>(ll * 2 + kv) * a.rows_p * a.dout;
+  const int64_t r = static_cast<int64_t>(tile) * kStageRows + i;
+  const int nb_n = a.dout / 32;
   const float* bb = a.bias[kv] + static_cast<int64_t>(l) * a.dout;
   float u1[8], u2[8];
 #pragma unroll
   for (int v = 0; v < 2; ++v) {
-    const float4 p1 = *reinterpret_cast<const float4*>(ur + o1 + 4 * v);
-    const float4 p2 = *reinterpret_cast<const float4*>(ur + o2 + 4 * v);
+    const float4 p1 = *reinterpret_cast<const float4*>(ub + ufrag(r, o1 + 4 * v, nb_n));
+    const float4 p2 = *reinterpret_cast<const float4*>(ub + ufrag(r, o2 + 4 * v, nb_n));
     const float4 c1 = *reinterpret_cast<const float4*>(bb + o1 + 4 * v);
     const float4 c2 = *reinterpret_cast<const float4*>(bb + o2 + 4 * v);
     u1[4 * v + 0] = p1.x + c1.x; u1[4 * v + 1] = p1.y + c1.y;
@@ -245,7 +298,9 @@ void launch_stage_pool(const StagedArgs& a, hipStream_t st) {
 }
 
 void launch_stage_project(const StagedArgs& a, hipStream_t st) {
-  stage_project<<<dim3(a.tiles, (a.dout + 127) / 128, a.nl * 2), dim3(256), 0, st>>>(a);
+  const int items = a.nl * 2 * a.tiles * ((a.dout + kProjCols - 1) / kProjCols);
+  const int per_xcd = (items + 7) / 8;
+  stage_project<<<dim3(per_xcd * 8), dim3(256), 0, st>>>(a, per_xcd);
 }
 
 void launch_stage_store(const StagedArgs& a, hipStream_t st) {
