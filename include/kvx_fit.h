@@ -115,17 +115,18 @@ kvx_status kvx_fit_reset(kvx_fit* fit, void* stream);
 int64_t kvx_fit_rows(const kvx_fit* fit);
 
 /* Diagnostics of a fit.  With the environment variable KVX_FIT_TIMING=1 at
- * accumulate time, every Gram-kernel launch is bracketed by HIP events on its
+ * accumulate time, every Gram pass (the K-system and the V-system launch of
+ * one group of target layers, back to back) is bracketed by HIP events on its
  * stream; kvx_fit_query then waits for them and reports their summed
  * duration (and releases them). */
 typedef struct {
   int32_t systems;        /* (target layer, K|V) systems = 2 * Lt */
   int32_t n;              /* unknowns per output column: din + fit_bias */
   int32_t gram_blocks;    /* 128 x 128 accumulator blocks per system */
-  int32_t gram_launches;  /* timed Gram launches since the last query */
+  int32_t gram_launches;  /* timed Gram passes since the last query */
   int64_t rows;           /* rows accumulated since create / reset */
   int64_t device_bytes;   /* accumulators and scratch currently held */
-  double gram_ms;         /* summed duration of the timed Gram launches, ms */
+  double gram_ms;         /* summed duration of the timed Gram passes, ms */
 } kvx_fit_info;
 
 kvx_status kvx_fit_query(kvx_fit* fit, kvx_fit_info* info);

@@ -4,9 +4,10 @@
 //
 // Device pipeline per batch of paired caches and group of target layers:
 //   fit_prepare  Z (pooled, source-de-rotated rows) and Y (target rows
-//                de-rotated by the target RoPE) as feature-major bf16 planes
-//                hi (and lo, unless the values are exact bf16),
-//                X^T[plane][feature][row]; adds the column sums of Z and Y
+//                de-rotated by the target RoPE) as bf16 planes hi (and lo,
+//                unless the values are exact bf16) of X^T[plane][feature][row],
+//                stored in matrix-core fragment order (xfrag); adds the
+//                column sums of Z and Y
 //                and the row count (the bias column's entries) to the
 //                accumulators;
 //   fit_gram     acc[i][j] += sum_r X[r][i] X[r][j] for i over the Z features
@@ -37,7 +38,17 @@ namespace {
 constexpr int kFB = 128;       // Gram block edge (features)
 constexpr int kSlab = 32;      // rows per LDS slab of the Gram kernel
 constexpr int kPrepRows = 64;  // rows per workgroup of fit_prepare (rows padded to it)
-constexpr int kPitch = kSlab + 8;  // LDS pitch (bf16) of one feature's slab row
+
+// X^T (features x rows, per plane) is stored in the order the Gram's MFMA
+// fragments read it: for each block of 32 features and each 16-row K step,
+// the 64 lanes' fragments (lane l: feature l % 32, rows 8 (l / 32) .. +7) as
+// one contiguous KiB.  A fragment is then one coalesced 1 KiB read, and a
+// 16-byte-per-lane copy of it into LDS lands lane-linear, so the waves'
+// fragment reads from LDS are free of bank conflicts.  Element offset of the
+// 8 rows r .. r+7 (r % 8 == 0) of feature f, rp rows per plane:
+__host__ __device__ constexpr int64_t xfrag(int64_t f, int64_t r, int64_t rp) {
+  return (((f / 32) * (rp / 16) + r / 16) * 64 + f % 32 + 32 * ((r / 8) % 2)) * 8;
+}
 constexpr int kFitBatch = 64;  // contexts per launch
 
 kvx_status fit_hip_fail(hipError_t e) { return hip_status(e); }
@@ -73,7 +84,7 @@ struct PrepArgs {
   int32_t tz, ty;          // job tiles of Z pairs and of Y pairs (then padding tiles)
   int32_t pz[2], py[2];    // planes written per K|V: 2 (hi, lo) or 1 (exact bf16)
   int32_t src_rope, tgt_rope, vec;
-  bf16_t* xt;  // [sys][2][F2][rp], sys = (l - l0) * 2 + kv
+  bf16_t* xt;  // [sys][2][F2 x rp in xfrag order], sys = (l - l0) * 2 + kv
   // bias sums (fit_bias): Z column sums into acc[sys][f][din], Y column sums
   // into acc[sys][din][din_p + c], the row count into acc[sys][din][din]
   float* acc;
@@ -151,8 +162,8 @@ __device__ __forceinline__ int tile_feature(const PrepArgs& a, int jt, int q) {
 
 // One workgroup: one job tile (128 features) x 64 rows of one system.  The
 // rows are formed token-major (16-byte loads of 8 pairs, 8 lanes per 128-byte
-// row segment), transposed through LDS, and written feature-major, 8 lanes per
-// 128-byte run of one feature; each feature's sum over the tile's rows goes to
+// row segment), transposed through LDS, and written in fragment order (xfrag),
+// 8 lanes per 128-byte run of 8 features; each feature's sum over the tile's rows goes to
 // the bias accumulators.  grid: (job tiles, rp / 64, systems of the group).
 template <typename T>
 __global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
@@ -296,7 +307,7 @@ __global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
       h[i] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
       lo[i] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
     }
-    bf16_t* dst = base + static_cast<int64_t>(f) * a.rp + r0 + 8 * oct;
+    bf16_t* dst = base + xfrag(f, r0 + 8 * oct, a.rp);
     *reinterpret_cast<uint4*>(dst) = make_uint4(h[0], h[1], h[2], h[3]);
     if (two) *reinterpret_cast<uint4*>(dst + plane) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
     if (a.fit_bias && oct == 0 && jt < a.tz + a.ty) {
@@ -311,27 +322,44 @@ __global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
 }
 
 struct GramArgs {
-  const bf16_t* xt;   // [sys][2][F2][rp]
+  const bf16_t* xt;   // [sys][2][F2 x rp in xfrag order]
   float* acc;         // [sys_total][din_p][F]; this group starts at sys0
   int32_t F2, rp, nbi, nbj, sys0, nblk;
   int32_t din_z, din_p, F;
   int32_t pz[2], py[2];  // operand planes per K|V (1: exact bf16, lo plane absent)
 };
 
+typedef __attribute__((address_space(3))) char lds_char;
+
 // One workgroup: one 128 x 128 block (bi, bj >= bi) of one system, all rows:
 // bi over the Z features, bj over Z and Y (the bias column's sums come from
-// fit_prepare).  Work items are system-major and each XCD takes a contiguous
+// fit_prepare).  One launch covers the K (kv = 0) or the V (kv = 1) systems
+// of a layer group, whose operands have PZ planes on the Z side and PY on the
+// Y side (1: exact bf16, lo plane absent), and LDS is sized for the planes
+// there are.  Work items are system-major and each XCD takes a contiguous
 // range, so the workgroups that re-read one system's operands share that
-// XCD's L2.  Four waves in 2 x 2, each 64 x 64 (2 x 2 MFMA tiles).  Slabs of
-// 32 rows of both feature blocks (hi and, for operands that have one, lo
-// planes) are staged through LDS, double buffered; the next slab is loaded
-// into registers during the MFMAs.  Products: hi*hi, plus hi*lo and lo*hi
-// when the B and the A operand have a lo plane (exact bf16 operands --
-// identity-aligned V, native V -- have none).
-__global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t sl[2][2][2][kFB * kPitch];  // [stage][A|B][plane]
+// XCD's L2.
+// Slabs of 32 rows (two K steps) of both feature blocks are copied from HBM
+// straight into LDS (16 bytes per lane, lane-linear: the fragments' own
+// order), kStages deep, the copy of slab s + kStages - 1 issued as slab s is
+// computed.  Four waves: wave pair p (0, 1) takes K step p of every slab and
+// each wave of a pair 64 of the block's rows x all 128 columns (2 x 4 MFMA
+// tiles), so a K step reads 6 fragments (per plane) for 8 tile products; the
+// pairs' partial sums are added through LDS at the end, in a fixed order.
+// Products: hi*hi, plus hi*lo and lo*hi when the B and the A operand have a
+// lo plane.
+constexpr int kStages = 2;
+
+template <int PZ, int PY>
+__global__ void __launch_bounds__(256, 2) fit_gram(GramArgs a, int kv) {
+  constexpr int PA = PZ, PB = PZ > PY ? PZ : PY;  // planes staged per side
+  constexpr int kChunk = 64 * 8;                  // bf16 of one fragment (1 KiB)
+  constexpr int kStage = (PA + PB) * 8 * kChunk;  // bf16 per slab: [A planes | B planes][4 fb][2 ks]
+  constexpr int kRed = 2 * 2 * 2 * 16 * 64;       // floats of one half of a pair's sums
+  constexpr int kBytes = kStages * kStage * 2 > kRed * 4 ? kStages * kStage * 2 : kRed * 4;
+  __shared__ __attribute__((aligned(16))) char lds[kBytes];
   const int wid = xcd_remap(blockIdx.x, gridDim.x);
-  const int sys = wid / a.nblk;
+  const int sys = 2 * (wid / a.nblk) + kv;  // system within the layer group
   int x = wid % a.nblk;
   int bi = 0;
   while (x >= a.nbj - bi) {
@@ -339,116 +367,118 @@ __global__ void __launch_bounds__(256) fit_gram(GramArgs a) {
     ++bi;
   }
   const int bj = bi + x;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-  const int wi = w / 2, wj = w % 2;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pk = w / 2, wi = w % 2;  // K step of the slab, 64-row half of the block
   const bf16_t* xs = a.xt + static_cast<int64_t>(sys) * 2 * a.F2 * a.rp;
   const int64_t plane = static_cast<int64_t>(a.F2) * a.rp;
-  const int kv = (a.sys0 + sys) % 2;
-  const bool lo_a = a.pz[kv] == 2;
-  const bool lo_b = (bj * kFB < a.din_z ? a.pz[kv] : a.py[kv]) == 2;
+  const int ksn = a.rp / 16;
+  constexpr bool lo_a = PZ == 2;
+  const bool lo_b = (bj * kFB < a.din_z ? PZ : PY) == 2;
 
-  // loader: piece p = tid + 256 * u (u < 2) of a 128-feature x 32-row slab
-  // plane: feature p / 4, 16-byte column p % 4; 2 blocks x 2 planes x 2.
-  // Two register sets: the loads of slab s + 2 are issued before the MFMAs
-  // of slab s, so they have about two slabs of compute to arrive.
-  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-  u32x4 ld[2][2][2][2];  // [set][A|B][plane][u]
-  auto load_slab = [&](int set, int r0) __attribute__((always_inline)) {
+  // copy of slab s into stage st: chunk c (wave w takes c = w + 4 m) is
+  // side A (c < 8 PA) or B, plane pl, feature block fbl, K step ksl
+  lds_char* const lds3 = (lds_char*)(lds);  // the LDS address space (sets M0 for the copies)
+  auto copy_slab = [&](int s, int st) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ab = 0; ab < 2; ++ab)
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl)
-        if (pl == 0 || (ab ? lo_b : lo_a))
-#pragma unroll
-          for (int u = 0; u < 2; ++u) {
-            const int p = tid + 256 * u;
-            const int f = (ab ? bj : bi) * kFB + p / 4;
-            ld[set][ab][pl][u] = *reinterpret_cast<const u32x4*>(
-                xs + pl * plane + static_cast<int64_t>(f) * a.rp + r0 + (p % 4) * 8);
-          }
-  };
-  auto store_slab = [&](int set, int st) __attribute__((always_inline)) {
-#pragma unroll
-    for (int ab = 0; ab < 2; ++ab)
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl)
-        if (pl == 0 || (ab ? lo_b : lo_a))
-#pragma unroll
-          for (int u = 0; u < 2; ++u) {
-            const int p = tid + 256 * u;
-            *reinterpret_cast<u32x4*>(&sl[st][ab][pl][(p / 4) * kPitch + (p % 4) * 8]) =
-                ld[set][ab][pl][u];
-          }
+    for (int m = 0; m < (PA + PB) * 2; ++m) {
+      const int c = w + 4 * m;
+      const bool isb = c >= PA * 8;
+      const int cc = isb ? c - PA * 8 : c;
+      const int pl = cc / 8, fbl = (cc % 8) / 2, ksl = cc % 2;
+      if (isb && pl == 1 && !lo_b) continue;
+      const int fb = (isb ? bj : bi) * 4 + fbl;
+      const bf16_t* g =
+          xs + pl * plane + (static_cast<int64_t>(fb) * ksn + 2 * s + ksl) * kChunk + lane * 8;
+      __builtin_amdgcn_global_load_lds(g, lds3 + (st * kStage + c * kChunk) * 2, 16, 0, 0);
+    }
   };
 
-  f32x16 acc[2][2];
+  f32x16 acc[2][4];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const int nslab = a.rp / kSlab;
-  load_slab(0, 0);
-  store_slab(0, 0);
-  if (nslab > 1) load_slab(1, kSlab);
+#pragma unroll
+  for (int s = 0; s + 1 < kStages; ++s)
+    if (s < nslab) copy_slab(s, s);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  // slab s: computed from LDS stage s % 2, loaded into register set s % 2
-  auto body = [&](int s, int set) __attribute__((always_inline)) {
-    const int st = s % 2;
-    if (s + 2 < nslab) load_slab(set, (s + 2) * kSlab);
+  const bf16x8* frag = reinterpret_cast<const bf16x8*>(lds);
+  for (int s = 0; s < nslab; ++s) {
+    const int st = s % kStages;
+    // this wave's fragments of the slab, then the next copy, then the MFMAs
+    bf16x8 fa[2][PA], fb[4][PB];
 #pragma unroll
-    for (int ks = 0; ks < kSlab / 16; ++ks) {
-      bf16x8 fa[2][2], fb[2][2];
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int pl = 0; pl < PA; ++pl)
+        fa[t][pl] = frag[(st * kStage) / 8 + ((pl * 4 + 2 * wi + t) * 2 + pk) * 64 + lane];
 #pragma unroll
-        for (int pl = 0; pl < 2; ++pl) {
-          if (pl == 0 || lo_a)
-            fa[t][pl] = *reinterpret_cast<const bf16x8*>(
-                &sl[st][0][pl][(wi * 64 + t * 32 + lane % 32) * kPitch + ks * 16 + 8 * (lane / 32)]);
-          if (pl == 0 || lo_b)
-            fb[t][pl] = *reinterpret_cast<const bf16x8*>(
-                &sl[st][1][pl][(wj * 64 + t * 32 + lane % 32) * kPitch + ks * 16 + 8 * (lane / 32)]);
-        }
-      // hi*hi, hi*lo, lo*hi (the last two for operands with a lo plane);
-      // consecutive MFMAs use different accumulators
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int term = 0; term < 3; ++term)
-        if (term == 0 || (term == 1 ? lo_b : lo_a))
+      for (int pl = 0; pl < PB; ++pl)
+        if (pl == 0 || lo_b)
+          fb[j][pl] = frag[(st * kStage) / 8 + (PA * 8 + (pl * 4 + j) * 2 + pk) * 64 + lane];
+    if (s + kStages - 1 < nslab) copy_slab(s + kStages - 1, (s + kStages - 1) % kStages);
+    // hi*hi, hi*lo, lo*hi; consecutive MFMAs use different accumulators
 #pragma unroll
-          for (int i = 0; i < 2; ++i)
+    for (int term = 0; term < 3; ++term)
+      if (term == 0 || (term == 1 ? lo_b : lo_a))
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                  fa[i][term == 2 ? 1 : 0], fb[j][term == 1 ? 1 : 0], acc[i][j], 0, 0, 0);
-    }
-    if (s + 1 < nslab) store_slab(set ^ 1, st ^ 1);
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                fa[i][term == 2 ? PA - 1 : 0], fb[j][term == 1 ? PB - 1 : 0], acc[i][j], 0, 0, 0);
+    // the copies of slab s + 1 have landed and every wave is done with stage st
+    // (the MFMAs stay before the wait: they are what hides the copies)
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-  };
-  int s = 0;
-  for (; s + 1 < nslab; s += 2) {
-    body(s, 0);
-    body(s + 1, 1);
   }
-  if (s < nslab) body(s, 0);
-  // D register v of lane l: row 8*(v/4) + 4*(l/32) + v%4, column l%32
+  // pair 1 hands its sums to pair 0 through LDS, half the columns at a time
+  // (lane-linear, [wi][i][jj][v][lane]); pair 0 adds them and updates the
+  // accumulators: D register v of lane l is row 8(v/4) + 4(l/32) + v%4,
+  // column l%32 of its tile
+  float* red = reinterpret_cast<float*>(lds);
   float* out = a.acc + static_cast<int64_t>(a.sys0 + sys) * a.din_p * a.F;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int h = 0; h < 2; ++h) {
+    if (pk == 1) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = bi * kFB + wi * 64 + i * 32 + 8 * (v / 4) + 4 * (lane / 32) + v % 4;
-        const int f = bj * kFB + wj * 64 + j * 32 + lane % 32;  // feature of X^T
-        const int col = f < a.din_z ? f : a.din_p + (f - a.din_z);
-        float* q = out + static_cast<int64_t>(row) * a.F + col;
-        *q += acc[i][j][v];
-      }
+        for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            red[(((wi * 2 + i) * 2 + jj) * 16 + v) * 64 + lane] = acc[i][2 * h + jj][v];
+    }
+    __syncthreads();
+    if (pk == 0) {
+      // per tile: its 16 accumulator loads first, then the stores
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const int f = bj * kFB + (2 * h + jj) * 32 + lane % 32;  // feature of X^T
+          const int col = f < a.din_z ? f : a.din_p + (f - a.din_z);
+          float* q = out + static_cast<int64_t>(bi * kFB + wi * 64 + i * 32 + 4 * (lane / 32)) * a.F + col;
+          float old[16];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) old[v] = q[static_cast<int64_t>(8 * (v / 4) + v % 4) * a.F];
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            q[static_cast<int64_t>(8 * (v / 4) + v % 4) * a.F] =
+                old[v] + (acc[i][2 * h + jj][v] + red[(((wi * 2 + i) * 2 + jj) * 16 + v) * 64 + lane]);
+        }
+    }
+    __syncthreads();
+  }
 }
 
 struct SolveArgs {
@@ -1113,8 +1143,21 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
         FIT_HIP(hipEventCreate(&ev[1]));
         FIT_HIP(hipEventRecord(ev[0], st));
       }
-      fit_gram<<<dim3(nblk * nl * 2), dim3(256), 0, st>>>(ga);
-      FIT_HIP(hipGetLastError());
+      // one launch for the K systems and one for the V systems of the group,
+      // each instantiated for its operands' planes
+      for (int kv = 0; kv < 2; ++kv) {
+        const dim3 gg(nblk * nl);
+        const int pz = planes_z[kv], py = planes_y[kv];
+        if (pz == 2 && py == 2)
+          fit_gram<2, 2><<<gg, dim3(256), 0, st>>>(ga, kv);
+        else if (pz == 2)
+          fit_gram<2, 1><<<gg, dim3(256), 0, st>>>(ga, kv);
+        else if (py == 2)
+          fit_gram<1, 2><<<gg, dim3(256), 0, st>>>(ga, kv);
+        else
+          fit_gram<1, 1><<<gg, dim3(256), 0, st>>>(ga, kv);
+        FIT_HIP(hipGetLastError());
+      }
       if (timing) {
         FIT_HIP(hipEventRecord(ev[1], st));
         f->timed.emplace_back(ev[0], ev[1]);
