@@ -341,14 +341,22 @@ typedef __attribute__((address_space(3))) char lds_char;
 // XCD's L2.
 // Slabs of 32 rows (two K steps) of both feature blocks are copied from HBM
 // straight into LDS (16 bytes per lane, lane-linear: the fragments' own
-// order), kStages deep, the copy of slab s + kStages - 1 issued as slab s is
-// computed.  Four waves: wave pair p (0, 1) takes K step p of every slab and
+// order), kSt deep (as many 16-32 KiB stages as fit 64 KiB, 2 to 4), the copy
+// of slab s + kSt - 1 issued as slab s is computed.  Four waves: wave pair p (0, 1) takes K step p of every slab and
 // each wave of a pair 64 of the block's rows x all 128 columns (2 x 4 MFMA
 // tiles), so a K step reads 6 fragments (per plane) for 8 tile products; the
 // pairs' partial sums are added through LDS at the end, in a fixed order.
 // Products: hi*hi, plus hi*lo and lo*hi when the B and the A operand have a
 // lo plane.
-constexpr int kStages = 2;
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding (LDS and export counters left alone)
+constexpr int vmcnt_le(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// Workgroup barrier for LDS hand-offs that leaves vector-memory operations in
+// flight (__syncthreads() would wait for all of them, the copies of later
+// slabs included); the memory clobber keeps the compiler's LDS accesses on
+// their side of it.
+__device__ __forceinline__ void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 template <int PZ, int PY>
 __global__ void __launch_bounds__(256, 2) fit_gram(GramArgs a, int kv) {
@@ -356,7 +364,10 @@ __global__ void __launch_bounds__(256, 2) fit_gram(GramArgs a, int kv) {
   constexpr int kChunk = 64 * 8;                  // bf16 of one fragment (1 KiB)
   constexpr int kStage = (PA + PB) * 8 * kChunk;  // bf16 per slab: [A planes | B planes][4 fb][2 ks]
   constexpr int kRed = 2 * 2 * 2 * 16 * 64;       // floats of one half of a pair's sums
-  constexpr int kBytes = kStages * kStage * 2 > kRed * 4 ? kStages * kStage * 2 : kRed * 4;
+  constexpr int kSt = 32768 / kStage < 2 ? 2 : (32768 / kStage > 4 ? 4 : 32768 / kStage);
+  constexpr int kBytes = kSt * kStage * 2 > kRed * 4 ? kSt * kStage * 2 : kRed * 4;
+  // copies per wave and slab (fewer when the B block has no lo plane)
+  constexpr int kCopies = (PA + PB) * 2 - (PB == 2 && PZ != PY ? 2 : 0);
   __shared__ __attribute__((aligned(16))) char lds[kBytes];
   const int wid = xcd_remap(blockIdx.x, gridDim.x);
   const int sys = 2 * (wid / a.nblk) + kv;  // system within the layer group
@@ -404,13 +415,18 @@ __global__ void __launch_bounds__(256, 2) fit_gram(GramArgs a, int kv) {
 
   const int nslab = a.rp / kSlab;
 #pragma unroll
-  for (int s = 0; s + 1 < kStages; ++s)
+  for (int s = 0; s + 1 < kSt; ++s)
     if (s < nslab) copy_slab(s, s);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  // slab 0 has landed: the copies of the kSt - 2 slabs after it may still be
+  // in flight, at least kCopies each; with fewer slabs, wait for all
+  if (nslab >= kSt - 1)
+    __builtin_amdgcn_s_waitcnt(vmcnt_le((kSt - 2) * kCopies));
+  else
+    __builtin_amdgcn_s_waitcnt(vmcnt_le(0));
+  lds_sync();
   const bf16x8* frag = reinterpret_cast<const bf16x8*>(lds);
   for (int s = 0; s < nslab; ++s) {
-    const int st = s % kStages;
+    const int st = s % kSt;
     // this wave's fragments of the slab, then the next copy, then the MFMAs
     bf16x8 fa[2][PA], fb[4][PB];
 #pragma unroll
@@ -424,7 +440,7 @@ __global__ void __launch_bounds__(256, 2) fit_gram(GramArgs a, int kv) {
       for (int pl = 0; pl < PB; ++pl)
         if (pl == 0 || lo_b)
           fb[j][pl] = frag[(st * kStage) / 8 + (PA * 8 + (pl * 4 + j) * 2 + pk) * 64 + lane];
-    if (s + kStages - 1 < nslab) copy_slab(s + kStages - 1, (s + kStages - 1) % kStages);
+    if (s + kSt - 1 < nslab) copy_slab(s + kSt - 1, (s + kSt - 1) % kSt);
     // hi*hi, hi*lo, lo*hi; consecutive MFMAs use different accumulators
 #pragma unroll
     for (int term = 0; term < 3; ++term)
@@ -435,12 +451,19 @@ __global__ void __launch_bounds__(256, 2) fit_gram(GramArgs a, int kv) {
           for (int j = 0; j < 4; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                 fa[i][term == 2 ? PA - 1 : 0], fb[j][term == 1 ? PB - 1 : 0], acc[i][j], 0, 0, 0);
-    // the copies of slab s + 1 have landed and every wave is done with stage st
-    // (the MFMAs stay before the wait: they are what hides the copies)
+    // the copies of slab s + 1 have landed and every wave is done with stage
+    // st.  While this iteration issued a copy, the kSt - 2 slabs after s + 1
+    // have theirs in flight, at least kCopies each, all issued after slab
+    // s + 1's; at the end, wait for all.  The MFMAs stay before the wait:
+    // they are what hides the copies.
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    if (s + kSt - 1 < nslab)
+      __builtin_amdgcn_s_waitcnt(vmcnt_le((kSt - 2) * kCopies));
+    else
+      __builtin_amdgcn_s_waitcnt(vmcnt_le(0));
+    lds_sync();
   }
+  __builtin_amdgcn_s_waitcnt(vmcnt_le(0));
   // pair 1 hands its sums to pair 0 through LDS, half the columns at a time
   // (lane-linear, [wi][i][jj][v][lane]); pair 0 adds them and updates the
   // accumulators: D register v of lane l is row 8(v/4) + 4(l/32) + v%4,
