@@ -37,7 +37,8 @@ namespace {
 
 constexpr int kFB = 128;       // Gram block edge (features)
 constexpr int kSlab = 32;      // rows per LDS slab of the Gram kernel
-constexpr int kPrepRows = 64;  // rows per workgroup of fit_prepare (rows padded to it)
+constexpr int kPrepRows = 64;   // rows per block of fit_prepare (rows padded to it)
+constexpr int kPrepBlocks = 4;  // row blocks per workgroup of fit_prepare
 
 // X^T (features x rows, per plane) is stored in the order the Gram's MFMA
 // fragments read it: for each block of 32 features and each 16-row K step,
@@ -160,34 +161,49 @@ __device__ __forceinline__ int tile_feature(const PrepArgs& a, int jt, int q) {
   return -1;
 }
 
-// One workgroup: one job tile (128 features) x 64 rows of one system.  The
-// rows are formed token-major (16-byte loads of 8 pairs, 8 lanes per 128-byte
-// row segment), transposed through LDS, and written in fragment order (xfrag),
-// 8 lanes per 128-byte run of 8 features; each feature's sum over the tile's rows goes to
-// the bias accumulators.  grid: (job tiles, rp / 64, systems of the group).
+// One workgroup: one job tile (128 features) x kPrepBlocks blocks of 64 rows
+// of one system.  Per block, the rows are formed token-major (16-byte loads of
+// 8 pairs, 8 lanes per 128-byte row segment), transposed through LDS, and
+// written in fragment order (xfrag), 8 lanes per 128-byte run of 8 features.
+// Each feature's sum over the workgroup's rows goes to the bias accumulators
+// in one atomic add.  grid: (job tiles, rp / (64 kPrepBlocks), systems of the
+// group).
 template <typename T>
-__global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
+__global__ void __launch_bounds__(256, 4) fit_prepare(PrepArgs a) {
   __shared__ float tr[128][65];  // [local feature][row]
-  const int jt = blockIdx.x, r0 = blockIdx.y * 64, sys = blockIdx.z;
+  const int jt = blockIdx.x, sys = blockIdx.z;
   const int l = a.l0 + sys / 2, kv = sys % 2;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const bool vec = a.vec != 0;
-  if (jt < a.tz + a.ty) {
-    const bool isz = jt < a.tz;
-    const int g = lane % 8;
-    const int npairs = isz ? a.din / 2 : a.dout / 2;
-    const int p0 = 64 * (isz ? jt : jt - a.tz) + 8 * g;  // 8 pairs of one head
-    const int half = (isz ? a.ds : a.dt) / 2;
-    const int hp = p0 / half, i0 = p0 % half;
-    const int j = hp / a.hs, hz = hp % a.hs;  // Z: mixed layer, source head
-    const T* zb = isz ? static_cast<const T*>(a.src[kv]) +
-                            a.layer_map[l * a.mix + (p0 < npairs ? j : 0)] * a.ss.l +
-                            hz * a.ss.h + i0
-                      : nullptr;
-    const T* yb = isz ? nullptr
-                      : static_cast<const T*>(a.tgt[kv]) + l * a.ts.l + hp * a.ts.h + i0;
-    const bool rot = kv == 0 && (isz ? a.src_rope : a.tgt_rope);
-    const double* fr = (isz ? a.fs : a.ft) + i0;
+  const int64_t plane = static_cast<int64_t>(a.F2) * a.rp;
+  bf16_t* base = a.xt + static_cast<int64_t>(sys) * 2 * plane;
+  float bsum[4] = {0.f, 0.f, 0.f, 0.f};  // this lane's octets of its 4 pieces, over the blocks
+  // the lane's 8 pairs (the same in every row block)
+  const bool isz = jt < a.tz;
+  const int g = lane % 8;
+  const int npairs = isz ? a.din / 2 : a.dout / 2;
+  const int p0 = 64 * (isz ? jt : jt - a.tz) + 8 * g;  // 8 pairs of one head
+  const int half = (isz ? a.ds : a.dt) / 2;
+  const int hp = p0 / half, i0 = p0 % half;
+  const int j = hp / a.hs, hz = hp % a.hs;  // Z: mixed layer, source head
+  const bool job = jt < a.tz + a.ty;
+  const T* zb = job && isz ? static_cast<const T*>(a.src[kv]) +
+                                 a.layer_map[l * a.mix + (p0 < npairs ? j : 0)] * a.ss.l +
+                                 hz * a.ss.h + i0
+                           : nullptr;
+  const T* yb = job && !isz ? static_cast<const T*>(a.tgt[kv]) + l * a.ts.l + hp * a.ts.h + i0
+                            : nullptr;
+  const bool rot = job && kv == 0 && (isz ? a.src_rope : a.tgt_rope);
+  // frequencies in registers (loads per use would wait behind the stores)
+  double fr[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) fr[q] = rot && p0 < npairs ? (isz ? a.fs : a.ft)[i0 + q] : 0.0;
+#pragma unroll 1
+  for (int rb = 0; rb < kPrepBlocks; ++rb) {
+  const int r0 = (blockIdx.y * kPrepBlocks + rb) * kPrepRows;
+  if (r0 >= a.rp) break;  // uniform
+  if (rb > 0) __syncthreads();  // the previous block's reads of tr are done
+  if (job) {
     if (!isz || !a.row_ptr) {
       // one row per unit (native target rows, identity-aligned source rows):
       // both units' loads are issued before either is used
@@ -276,11 +292,8 @@ __global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
     for (int idx = tid; idx < 128 * 64; idx += 256) tr[idx / 64][idx % 64] = 0.f;
   }
   __syncthreads();
-  // feature-major output: piece = (local feature, 8-row octet)
-  const int64_t plane = static_cast<int64_t>(a.F2) * a.rp;
-  bf16_t* base = a.xt + static_cast<int64_t>(sys) * 2 * plane;
-  float* acc = a.acc + static_cast<int64_t>(a.sys0 + sys) * a.din_p * a.F;
-#pragma unroll 1
+  // fragment-order output: piece = (local feature, 8-row octet)
+#pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int piece = tid + 256 * k;
     const int q = piece / 8, oct = piece % 8;
@@ -288,13 +301,8 @@ __global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
     float v[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = tr[q][8 * oct + e];
-    // sum over the tile's 64 rows: the 8 lanes of one feature are adjacent
-    float sum = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) sum += v[e];
-    sum += __shfl_xor(sum, 1);
-    sum += __shfl_xor(sum, 2);
-    sum += __shfl_xor(sum, 4);
+    for (int e = 0; e < 8; ++e) bsum[k] += v[e];
     if (f < 0) continue;
     const bool zf = f < a.din_z;
     const bool two = (zf ? a.pz[kv] : a.py[kv]) == 2;
@@ -310,14 +318,26 @@ __global__ void __launch_bounds__(256) fit_prepare(PrepArgs a) {
     bf16_t* dst = base + xfrag(f, r0 + 8 * oct, a.rp);
     *reinterpret_cast<uint4*>(dst) = make_uint4(h[0], h[1], h[2], h[3]);
     if (two) *reinterpret_cast<uint4*>(dst + plane) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-    if (a.fit_bias && oct == 0 && jt < a.tz + a.ty) {
-      if (zf)
-        atomicAdd(acc + static_cast<int64_t>(f) * a.F + a.din, sum);
-      else
-        atomicAdd(acc + static_cast<int64_t>(a.din) * a.F + a.din_p + (f - a.din_z), sum);
-    }
   }
-  if (a.fit_bias && jt == 0 && blockIdx.y == 0 && tid == 0)
+  }
+  if (!a.fit_bias) return;
+  // each feature's sum over the workgroup's rows: its 8 octet lanes are adjacent
+  float* acc = a.acc + static_cast<int64_t>(a.sys0 + sys) * a.din_p * a.F;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    float sum = bsum[k];
+    sum += __shfl_xor(sum, 1);
+    sum += __shfl_xor(sum, 2);
+    sum += __shfl_xor(sum, 4);
+    const int piece = tid + 256 * k;
+    const int f = tile_feature(a, jt, piece / 8);
+    if (f < 0 || piece % 8 != 0 || jt >= a.tz + a.ty) continue;
+    if (f < a.din_z)
+      atomicAdd(acc + static_cast<int64_t>(f) * a.F + a.din, sum);
+    else
+      atomicAdd(acc + static_cast<int64_t>(a.din) * a.F + a.din_p + (f - a.din_z), sum);
+  }
+  if (jt == 0 && blockIdx.y == 0 && tid == 0)
     atomicAdd(acc + static_cast<int64_t>(a.din) * a.F + a.din, static_cast<float>(a.nrows));
 }
 
@@ -1136,7 +1156,8 @@ kvx_status kvx_fit_accumulate(kvx_fit* f, const kvx_fit_io* io_in, void* stream)
       pa.fit_bias = f->fit_bias;
       pa.ctx = ctx;
       const int npad = (f->din_z - f->din) + (f->dout_p - f->dout);
-      const dim3 pg(pa.tz + pa.ty + (npad + 127) / 128, rp / kPrepRows, nl * 2);
+      const int rows_wg = kPrepRows * kPrepBlocks;
+      const dim3 pg(pa.tz + pa.ty + (npad + 127) / 128, (rp + rows_wg - 1) / rows_wg, nl * 2);
       if (f->dtype == KVX_F32)
         fit_prepare<float><<<pg, dim3(256), 0, st>>>(pa);
       else

@@ -122,6 +122,31 @@ def test_fit_qwen_heads_outliers():
     _compare(prob, tk, tv, got, 2.0, True, 2e-2, "qwen")
 
 
+def test_fit_unaligned_caches():
+    """Caches that start 2 bytes past a 16-byte boundary: the fit reads them
+    element by element instead of in 16-byte loads, with the same result."""
+    T = U.torch()
+    prob = S.make_problem(_spec(src_tokens=150))
+    tk, tv = _native(prob, noise=0.05)
+    spec = prob.spec
+
+    def shifted(a):
+        d = U.np_to_dev(a, spec.dtype)
+        flat = T.empty(d.numel() + 8, dtype=d.dtype, device="cuda")
+        v = flat[1:1 + d.numel()].view(d.shape)
+        v.copy_(d)
+        assert v.data_ptr() % 16 != 0
+        return v
+
+    print("[fit] unaligned caches", flush=True)
+    fitter = kvx.Fitter(spec.src, spec.tgt, spec.mix, spec.layer_map, kvx.KVX_BF16, True)
+    fitter.accumulate(shifted(prob.src_k), shifted(prob.src_v), shifted(tk), shifted(tv))
+    got = [x.cpu().numpy().astype(np.float64) for x in fitter.solve(1.0)]
+    T.cuda.synchronize()
+    fitter.close()
+    _compare(prob, tk, tv, got, 1.0, True, 1e-3, "unaligned")
+
+
 def test_fit_f32_without_bias():
     spec = _spec(dtype=S.F32, bias_std=0.0, src_tokens=200)
     prob = S.make_problem(spec)
