@@ -133,67 +133,97 @@ __global__ void __launch_bounds__(256) stage_pool(StagedArgs a) {
 
 // Stage 2.  One work item: 128 rows x 256 outputs of one (target layer,
 // K|V) system, on 4 waves of 64 rows x 128 outputs (2 x 4 tiles of
-// v_mfma_f32_32x32x16_bf16).  Fragments come straight from memory as
-// contiguous KiB reads -- Z in fragment order, the plan's packed weights --
-// kPrefetch - 1 K steps ahead of the MFMAs that use them.  The 1-D grid is
-// laid out for the 8 XCDs: workgroup n runs on XCD n % 8, so n is mapped to
-// work item (n % 8) * per_xcd + n / 8 and each XCD walks one contiguous run
-// of items (system-major, then row tile, then output tile): the items
-// sharing a row tile, and the row tiles sharing a system's weights, run
-// together on one L2.
-constexpr int kProjRows = 128, kProjCols = 256, kPrefetch = 3;
+// v_mfma_f32_32x32x16_bf16).  Z (in fragment order) and the plan's packed
+// weights are copied slab by slab (two K steps: per plane 4 row blocks, and
+// 8 output blocks, of 1 KiB fragments) from HBM straight into LDS with
+// 16-byte-per-lane loads, which land lane-linear: the waves then read their
+// fragments from LDS without bank conflicts, each fragment fetched from
+// memory once per workgroup instead of once per wave.  Two stages: the copy
+// of slab s + 1 is issued while slab s is contracted.  The 1-D grid is laid
+// out for the 8 XCDs: workgroup n runs on XCD n % 8, so n is mapped to work
+// item (n % 8) * per_xcd + n / 8 and each XCD walks one contiguous run of
+// items (system-major, then row tile, then output tile): the items sharing a
+// row tile, and the row tiles sharing a system's weights, run together on
+// one L2.
+constexpr int kProjRows = 128, kProjCols = 256;
+constexpr int kProjChunks = 32;  // 1 KiB fragments per slab stage: A [2 planes][4][2], B [8][2]
 
-// The K steps of one wave's 64 x 128 tile; TWO: the operand has a lo plane.
-// Output blocks past dout (nbv < 4) are computed against the last block's
-// weights and not stored.
+typedef __attribute__((address_space(3))) char lds_char;
+
+// Workgroup barrier for LDS hand-offs that leaves vector-memory operations in
+// flight; the memory clobber keeps the compiler's LDS accesses on their side.
+__device__ __forceinline__ void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// The slabs of one work item; TWO: the operand has a lo plane.  Output blocks
+// past dout (nbv < 4) are computed against the last block's weights and not
+// stored.
 template <bool TWO>
-__device__ __forceinline__ void project_steps(const bf16x8* const (&zrow)[2], int64_t plane8,
-                                              const bf16x8* const (&wb)[4], int ks_n,
-                                              f32x16 (&acc)[2][4]) {
-  struct Frag {
-    bf16x8 A[2][TWO ? 2 : 1], B[4];
-  };
-  auto load = [&](Frag& f, int ks) __attribute__((always_inline)) {
+__device__ __forceinline__ void project_slabs(const bf16_t* zb, int64_t plane, const bf16x8* wl,
+                                              int rb0, int nb0w, int nb_n, int ks_n, int wi,
+                                              int wj, bf16x8* lds, f32x16 (&acc)[2][4]) {
+  constexpr int P = TWO ? 2 : 1;
+  const int lane = threadIdx.x % 64;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+  const int nb0 = nb0w - 4 * wj;  // first output block of the work item
+  lds_char* const l3 = (lds_char*)(lds);
+  // chunk c (wave w copies c = w + 4 m): A chunks (pl, row block, K step) at
+  // (pl * 4 + rbl) * 2 + ksl, B chunks (output block, K step) at 16 + nbl * 2 + ksl
+  auto copy_slab = [&](int s, int st) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      f.A[i][0] = zrow[i][ks * 64];
-      if constexpr (TWO) f.A[i][1] = zrow[i][plane8 + ks * 64];
-    }
-#pragma unroll
-    for (int jb = 0; jb < 4; ++jb) f.B[jb] = wb[jb][ks * 64];
-  };
-  auto mma = [&](const Frag& f) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int jb = 0; jb < 4; ++jb) {
-        acc[i][jb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.A[i][0], f.B[jb], acc[i][jb], 0, 0, 0);
-        if constexpr (TWO)
-          acc[i][jb] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.A[i][1], f.B[jb], acc[i][jb], 0, 0, 0);
+    for (int m = 0; m < (8 * P + 16) / 4; ++m) {
+      const int c = w + 4 * m;
+      const bool isb = c >= 8 * P;
+      const int cc = isb ? c - 8 * P : c;
+      const int slot = isb ? 16 + cc : cc;
+      const void* g;
+      if (isb) {
+        const int nb = min(nb0 + cc / 2, nb_n - 1);
+        g = wl + (static_cast<int64_t>(nb) * ks_n + 2 * s + cc % 2) * 64 + lane;
+      } else {
+        const int pl = cc / 8, rbl = (cc % 8) / 2;
+        g = zb + pl * plane + ((static_cast<int64_t>(rb0 + rbl) * ks_n + 2 * s + cc % 2) * 64 + lane) * 8;
       }
-  };
-  Frag f[kPrefetch];
-#pragma unroll
-  for (int s = 0; s + 1 < kPrefetch; ++s)
-    if (s < ks_n) load(f[s], s);
-  for (int k0 = 0; k0 < ks_n; k0 += kPrefetch) {
-#pragma unroll
-    for (int s = 0; s < kPrefetch; ++s) {
-      const int ks = k0 + s;
-      if (ks < ks_n) {
-        // refill the buffer the previous step consumed
-        if (ks + kPrefetch - 1 < ks_n) load(f[(s + kPrefetch - 1) % kPrefetch], ks + kPrefetch - 1);
-        mma(f[s]);
-      }
+      __builtin_amdgcn_global_load_lds(g, l3 + (st * kProjChunks + slot) * 1024, 16, 0, 0);
     }
+  };
+  const int nslab = ks_n / 2;
+  copy_slab(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  lds_sync();
+  for (int s = 0; s < nslab; ++s) {
+    const bf16x8* f = lds + (s % 2) * kProjChunks * 64;
+#pragma unroll
+    for (int ksl = 0; ksl < 2; ++ksl) {
+      bf16x8 fa[2][P], fb[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int pl = 0; pl < P; ++pl) fa[i][pl] = f[((pl * 4 + 2 * wi + i) * 2 + ksl) * 64 + lane];
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) fb[jb] = f[(16 + (4 * wj + jb) * 2 + ksl) * 64 + lane];
+      if (ksl == 0 && s + 1 < nslab) copy_slab(s + 1, (s + 1) % 2);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb) {
+          acc[i][jb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i][0], fb[jb], acc[i][jb], 0, 0, 0);
+          if constexpr (TWO)
+            acc[i][jb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i][1], fb[jb], acc[i][jb], 0, 0, 0);
+        }
+    }
+    // slab s + 1 has landed and every wave is done with this stage (the
+    // MFMAs stay before the wait)
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    lds_sync();
   }
 }
 
 __global__ void __launch_bounds__(256, 2) stage_project(StagedArgs a, int per_xcd) {
+  __shared__ __attribute__((aligned(16))) bf16x8 lds[2 * kProjChunks * 64];  // 64 KiB
   const int item = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
   const int n_ct = (a.dout + kProjCols - 1) / kProjCols;
-  if (item >= a.nl * 2 * a.tiles * n_ct) return;  // no barrier in this kernel
+  if (item >= a.nl * 2 * a.tiles * n_ct) return;  // whole workgroup: before any barrier
   const int ct = item % n_ct, tile = item / n_ct % a.tiles, sys = item / n_ct / a.tiles;
   const int ll = sys / 2, kv = sys % 2, l = a.l0 + ll;
   const int lane = threadIdx.x % 64, w = threadIdx.x / 64;
@@ -201,11 +231,9 @@ __global__ void __launch_bounds__(256, 2) stage_project(StagedArgs a, int per_xc
   const int nb_n = a.dout / 32, ks_n = a.din / 16;
   const int nb0 = ct * (kProjCols / 32) + wj * 4;  // first 32-output block of this wave
   const int nbv = min(4, nb_n - nb0);
-  if (nbv <= 0) return;
   const int64_t plane = static_cast<int64_t>(a.rows_p) * a.din;
   const bf16_t* zb = a.z + static_cast<int64_t>(ll * 2 + kv) * 2 * plane;
   const bf16x8* wl = a.wp[kv] + static_cast<int64_t>(l) * nb_n * ks_n * 64;
-  const int r0 = tile * kProjRows + wi * 64;
   f32x16 acc[2][4];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -213,21 +241,14 @@ __global__ void __launch_bounds__(256, 2) stage_project(StagedArgs a, int per_xc
     for (int jb = 0; jb < 4; ++jb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][jb][v] = 0.f;
-  // A fragment of row block i at K step ks: zrow[i][ks * 64], lo plane + plane8
-  const bf16x8* zrow[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-    zrow[i] =
-        reinterpret_cast<const bf16x8*>(zb + zfrag(r0 + 32 * i + lane % 32, 8 * (lane / 32), ks_n));
-  const bf16x8* wb[4];
-#pragma unroll
-  for (int jb = 0; jb < 4; ++jb)
-    wb[jb] = wl + static_cast<int64_t>(min(nb0 + jb, nb_n - 1)) * ks_n * 64 + lane;
+  // every wave takes part in the copies and barriers, also one whose
+  // output blocks are all past dout (it stores nothing)
   if (a.planes[kv] == 2)
-    project_steps<true>(zrow, plane / 8, wb, ks_n, acc);
+    project_slabs<true>(zb, plane, wl, tile * 4, nb0, nb_n, ks_n, wi, wj, lds, acc);
   else
-    project_steps<false>(zrow, plane / 8, wb, ks_n, acc);
+    project_slabs<false>(zb, plane, wl, tile * 4, nb0, nb_n, ks_n, wi, wj, lds, acc);
   // U in D-fragment order: register v of every lane is 256 contiguous bytes
+  const int r0 = tile * kProjRows + wi * 64;
   float* ub = a.u + static_cast<int64_t>(ll * 2 + kv) * a.rows_p * a.dout;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
