@@ -64,6 +64,19 @@ def test_staged_single_bf16_operands():
     _check(S.config(3, src_tokens=600), precision=kvx.KVX_PREC_BF16)
 
 
+def test_staged_output_width_not_multiple_of_256():
+    """dout = 384 (three target heads of 128): the projection's last work item
+    covers 128 outputs, so one of its waves has no output block to store and
+    only takes part in the copies and barriers; a span map with two mixed
+    source layers on top."""
+    spec = S.Spec(cfg_id=401, name="staged-384", src=S.ModelShape(4, 2, 64, 1.0e4),
+                  tgt=S.ModelShape(3, 3, 128, 1.0e6), mix=2, layer_map=(0, 1, 1, 2, 3, 2),
+                  dtype=S.BF16, src_tokens=330, batch=2, span_lo=1, span_hi=3, bias_std=0.2,
+                  seed=5)
+    assert spec.d_out % 256 == 128 and spec.d_in % 128 == 0
+    _check(spec)
+
+
 def test_staged_layer_groups():
     """A workspace for 3 layers: the call runs the 28 layers in groups."""
     _check(S.config(2, src_tokens=200), layers=3)
